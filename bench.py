@@ -1,0 +1,212 @@
+#!/usr/bin/env python3
+"""Throughput of libdconv on one MI355X.
+
+A step is one pass of the direct-convolution hot path over one batch of
+synthetic input.  The default workload is the single-map 4096 x 4096 input
+with one filter, swept over K = 3, 5, 7, 9, 11 (five dconv_single launches per
+step, each with its own input and output buffers so that one step touches
+670 MB, more than the 256 MB Infinity Cache, and every launch reads its input
+from HBM).  ``--workload`` selects any other named workload (multi-channel
+shapes are measured the same way, one launch per step).
+
+Prints ONE JSON line: GFLOP/s over the timed steps (2*C*M*K^2*Hout*Wout
+flops per launch), the roofline of the dominant kernel measured with HIP
+events on the launch stream, and the CPU oracle timed on the host cores.
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+METRIC = "GFLOP/s and % fp32 roofline for dconv_single/dconv_multi (fp32, 1 MI355X)"
+PEAK_FP32_VECTOR_TFLOPS = 157.3      # 256 CU x 2.4 GHz x 256 flop/clk (packed FMA)
+PEAK_FP32_UNPACKED_TFLOPS = 78.6     # one fp32 FMA per lane per clock
+PEAK_FP32_MFMA_TFLOPS = 157.3
+PEAK_HBM_GBS = 8000.0
+SWEEP = "single_4096x4096_m1_k3-11"
+
+
+def parse():
+    ap = argparse.ArgumentParser(description=__doc__)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=50)
+    ap.add_argument("--warmup", type=int, default=5)
+    ap.add_argument("--workload", default=SWEEP,
+                    help="%s (default) or a name from dconv_workloads.WORKLOADS" % SWEEP)
+    ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "valu"],
+                    help="kernel family for multi-channel workloads")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-reps", type=int, default=2)
+    return ap.parse_args()
+
+
+def traffic_for(kernel_tag):
+    """HBM bytes per launch measured with rocprofv3 counters, if recorded
+    for the current kernel sources (profiles/traffic.json); else None."""
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.json")
+    if not os.path.exists(path):
+        return None
+    try:
+        data = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    ent = data.get(kernel_tag)
+    if not ent:
+        return None
+    from paper_2212_00404_amd.build import source_digest
+    if ent.get("source_digest") != source_digest():
+        return None
+    return ent.get("bytes_per_launch")
+
+
+def cpu_baseline(launches, reps):
+    """The fp64 oracle on the host cores over the same launches (whole step)."""
+    import oracle
+    threads = int(os.environ.get("OMP_NUM_THREADS") or 0) or oracle.default_threads()
+    flops = sum(w.flops for w, _, _ in launches)
+    best = None
+    for _ in range(max(1, reps)):
+        t0 = time.perf_counter()
+        for w, I, F in launches:
+            if w.kind == "single":
+                oracle.conv_single(I, F, threads=threads)
+            else:
+                oracle.conv_multi(I, F, threads=threads)
+        dt = time.perf_counter() - t0
+        best = dt if best is None else min(best, dt)
+    return {"value": round(flops / best / 1e9, 3), "unit": "GFLOP/s", "cores": threads,
+            "kind": "oracle",
+            "sample": "one full step (%d launch%s, %.2f GFLOP), best of %d, fp64 C oracle"
+                      % (len(launches), "es" if len(launches) > 1 else "", flops / 1e9, reps)}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py measures one GPU: this build has no multi-GPU path "
+              "(run with --gpus 1)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2212_00404_amd as dc
+    from dconv_workloads import SINGLE_4096_SWEEP, WORKLOADS, make
+
+    names = list(SINGLE_4096_SWEEP) if args.workload == SWEEP else [args.workload]
+    for n in names:
+        if n not in WORKLOADS:
+            sys.exit("unknown workload %s" % n)
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    dc.load()
+
+    launches = []   # (workload, host I, host F)
+    bufs = []       # (workload, I, F, O) on the device
+    for n in names:
+        w = WORKLOADS[n]
+        I, F = make(w)
+        launches.append((w, I, F))
+        It = torch.from_numpy(I).to(dev)
+        Ft = torch.from_numpy(F).to(dev)
+        Ot = torch.empty((w.M, w.Hout, w.Wout), dtype=torch.float32, device=dev)
+        bufs.append((w, It, Ft, Ot))
+    torch.cuda.synchronize()
+
+    def launch(b):
+        w, It, Ft, Ot = b
+        if w.kind == "single":
+            dc.single(It, Ft, out=Ot)
+        else:
+            dc.multi(It, Ft, out=Ot, variant=args.variant)
+
+    for _ in range(args.warmup):
+        for b in bufs:
+            launch(b)
+    torch.cuda.synchronize()
+
+    # Timed region: HIP events around every launch, on the launch stream.
+    stream = torch.cuda.current_stream(dev)
+    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in bufs] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    start = torch.cuda.Event(enable_timing=True)
+    stop = torch.cuda.Event(enable_timing=True)
+    start.record(stream)
+    for s in range(args.steps):
+        for i, b in enumerate(bufs):
+            ev[s][i][0].record(stream)
+            launch(b)
+            ev[s][i][1].record(stream)
+    stop.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    total_ms = start.elapsed_time(stop)
+    ms_per_step = total_ms / args.steps
+
+    step_flops = sum(w.flops for w, _, _, _ in bufs)
+    value_gflops = step_flops / (ms_per_step * 1e-3) / 1e9
+
+    per_kernel = []
+    for i, (w, _, _, _) in enumerate(bufs):
+        d = np.array([ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)])
+        avg_s = float(d.mean()) * 1e-3
+        tf = w.flops / avg_s / 1e12
+        gbs = w.compulsory_bytes / avg_s / 1e9
+        ai = w.flops / w.compulsory_bytes
+        per_kernel.append({
+            "workload": w.name, "avg_us": round(avg_s * 1e6, 2),
+            "median_us": round(float(np.median(d)) * 1e3, 2),
+            "tflops": round(tf, 2), "gbs": round(gbs, 1), "flop_per_byte": round(ai, 2),
+            "frac_fp32_peak": round(tf / PEAK_FP32_VECTOR_TFLOPS, 4),
+            "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
+
+    dom = max(range(len(bufs)), key=lambda i: per_kernel[i]["avg_us"])
+    w = bufs[dom][0]
+    pk = per_kernel[dom]
+    ridge_unpacked = PEAK_FP32_UNPACKED_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
+    uses_mfma = (w.kind == "multi" and
+                 dc.plan_multi(w.C, w.M, w.Wx, w.Wy, w.K, args.variant)["variant"] == 2)
+    compute_bound = (w.flops / w.compulsory_bytes) >= ridge_unpacked
+    tag = "%s/%s" % (w.name, args.variant if w.kind == "multi" else "single")
+    traffic = traffic_for(tag)
+    if compute_bound:
+        achieved = w.flops / (pk["avg_us"] * 1e-6) / 1e12
+        peak = PEAK_FP32_MFMA_TFLOPS if uses_mfma else PEAK_FP32_VECTOR_TFLOPS
+        roof = {"bound": "mfma" if uses_mfma else "alu", "achieved": round(achieved, 2),
+                "peak": peak, "unit": "TFLOP/s", "frac": round(achieved / peak, 4),
+                "traffic": traffic, "kernel": w.name,
+                "flops_per_launch": w.flops,
+                "peak_unpacked_fp32": None if uses_mfma else PEAK_FP32_UNPACKED_TFLOPS}
+    else:
+        achieved = w.compulsory_bytes / (pk["avg_us"] * 1e-6) / 1e9
+        roof = {"bound": "hbm", "achieved": round(achieved, 1), "peak": PEAK_HBM_GBS,
+                "unit": "GB/s", "frac": round(achieved / PEAK_HBM_GBS, 4),
+                "traffic": traffic, "kernel": w.name,
+                "bytes_per_launch": w.compulsory_bytes}
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(launches, args.cpu_reps)
+
+    if args.workload == SWEEP:
+        config = {"workload": SWEEP, "kind": "single", "Wx": 4096, "Wy": 4096, "M": 1, "C": 1,
+                  "K": [3, 5, 7, 9, 11], "launches_per_step": 5,
+                  "buffers": "separate I/O per K (670 MB per step)"}
+    else:
+        config = {"workload": w.name, "kind": w.kind, "C": w.C, "M": w.M, "Wx": w.Wx,
+                  "Wy": w.Wy, "K": w.K, "variant": args.variant, "launches_per_step": 1}
+    out = {
+        "metric": METRIC, "value": round(value_gflops, 2), "unit": "GFLOP/s", "n_gpus": 1,
+        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
+        "data": "synthetic", "config": config, "roofline": roof, "cpu_baseline": cpu,
+        "per_kernel": per_kernel, "wall_s_timed": round(wall, 4),
+    }
+    print(json.dumps(out), flush=True)
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,180 @@
+// C ABI of libdconv: argument validation, planning and launch (the host side
+// of the library; the kernels live in single.hip and multi.hip).
+//
+// Every entry point validates its arguments before touching the HIP runtime,
+// so NULL pointers and bad sizes are reported without a device.
+#include <climits>
+#include <cstdint>
+#include <mutex>
+#include <vector>
+
+#include "internal.h"
+
+#define DCONV_EXPORT extern "C" __attribute__((visibility("default")))
+
+namespace {
+
+// Compute-unit count per device, read once per process; immutable afterwards.
+std::once_flag g_props_once;
+std::vector<int> g_num_cu;
+
+void read_props() {
+  int n = 0;
+  if (hipGetDeviceCount(&n) != hipSuccess || n < 0) n = 0;
+  g_num_cu.assign(n, 0);
+  for (int d = 0; d < n; ++d) {
+    int cu = 0;
+    if (hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, d) == hipSuccess)
+      g_num_cu[d] = cu;
+  }
+  (void)hipGetLastError();
+}
+
+// Returns DCONV_OK and the current device's CU count, or DCONV_EHIP.
+int current_num_cu(int *num_cu) {
+  std::call_once(g_props_once, read_props);
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return DCONV_EHIP;
+  }
+  if (dev < 0 || dev >= (int)g_num_cu.size() || g_num_cu[dev] <= 0) return DCONV_EHIP;
+  *num_cu = g_num_cu[dev];
+  return DCONV_OK;
+}
+
+// Sizes of Eq. 1: C, M, K >= 1, 1 <= K <= min(Wx, Wy) (valid mode needs at
+// least one output), and every tensor indexable with 32-bit element offsets.
+int validate_sizes(int C, int M, int Wx, int Wy, int K) {
+  if (C < 1 || M < 1 || K < 1 || Wx < 1 || Wy < 1 || K > Wx || K > Wy) return DCONV_EINVAL;
+  const int64_t Hout = (int64_t)Wy - K + 1;
+  const int64_t Wout = (int64_t)Wx - K + 1;
+  const int64_t in = (int64_t)C * Wy * Wx;
+  const int64_t f = (int64_t)M * C * K * K;
+  const int64_t out = (int64_t)M * Hout * Wout;
+  if (in > INT_MAX || f > INT_MAX || out > INT_MAX) return DCONV_ERANGE;
+  return DCONV_OK;
+}
+
+void export_single(const dconv::SinglePlan &p, dconv_plan *out) {
+  *out = dconv_plan{};
+  out->variant = DCONV_VARIANT_VALU;
+  out->kernel = p.kernel;
+  out->tile_m = p.m_per_block;
+  out->tile_h = p.tile_h;
+  out->tile_w = p.tile_w;
+  out->chunk_c = 1;
+  out->split_c = 1;
+  out->grid_x = p.grid;
+  out->grid_y = p.grid_z;
+  out->grid_z = 1;
+  out->block = p.block;
+  out->lds_bytes = p.lds_bytes;
+  out->workspace_bytes = 0;
+}
+
+void export_multi(const dconv::MultiPlan &p, dconv_plan *out) {
+  *out = dconv_plan{};
+  out->variant = p.variant;
+  out->kernel = p.kernel;
+  out->tile_m = p.tile_m;
+  out->tile_h = p.tpy;
+  out->tile_w = p.tpx;
+  out->chunk_c = p.chunk_c;
+  out->split_c = p.split_c;
+  out->grid_x = p.grid_x;
+  out->grid_y = p.grid_y;
+  out->grid_z = p.grid_z;
+  out->block = p.block;
+  out->lds_bytes = p.lds_bytes;
+  out->workspace_bytes = p.workspace_bytes;
+}
+
+}  // namespace
+
+DCONV_EXPORT int dconv_single(const float *I, const float *F, float *O, int Wx, int Wy, int K,
+                              int M, void *stream) {
+  if (!I || !F || !O) return DCONV_ENULL;
+  int rc = validate_sizes(1, M, Wx, Wy, K);
+  if (rc != DCONV_OK) return rc;
+  int num_cu = 0;
+  if ((rc = current_num_cu(&num_cu)) != DCONV_OK) return rc;
+  dconv::SinglePlan p;
+  dconv::plan_single(Wx, Wy, K, M, num_cu, &p);
+  const hipError_t e = dconv::launch_single(p, I, F, O, Wx, Wy, M, (hipStream_t)stream);
+  return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
+}
+
+DCONV_EXPORT int dconv_multi_variant(const float *I, const float *F, float *O, int C, int M,
+                                     int Wx, int Wy, int K, int variant, void *stream) {
+  if (!I || !F || !O) return DCONV_ENULL;
+  if (variant != DCONV_VARIANT_AUTO && variant != DCONV_VARIANT_VALU &&
+      variant != DCONV_VARIANT_MFMA)
+    return DCONV_EINVAL;
+  int rc = validate_sizes(C, M, Wx, Wy, K);
+  if (rc != DCONV_OK) return rc;
+  int num_cu = 0;
+  if ((rc = current_num_cu(&num_cu)) != DCONV_OK) return rc;
+  dconv::MultiPlan p;
+  if ((rc = dconv::plan_multi(C, M, Wx, Wy, K, variant, num_cu, &p)) != DCONV_OK) return rc;
+  hipStream_t st = (hipStream_t)stream;
+  float *ws = nullptr;
+  if (p.workspace_bytes > 0) {
+    if (hipMallocAsync((void **)&ws, (size_t)p.workspace_bytes, st) != hipSuccess) {
+      (void)hipGetLastError();
+      return DCONV_ENOMEM;
+    }
+  }
+  const hipError_t e = dconv::launch_multi(p, I, F, O, ws, C, M, Wx, Wy, st);
+  if (ws) {
+    if (hipFreeAsync(ws, st) != hipSuccess) {
+      (void)hipGetLastError();
+      return DCONV_EHIP;
+    }
+  }
+  return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
+}
+
+DCONV_EXPORT int dconv_multi(const float *I, const float *F, float *O, int C, int M, int Wx,
+                             int Wy, int K, void *stream) {
+  return dconv_multi_variant(I, F, O, C, M, Wx, Wy, K, DCONV_VARIANT_AUTO, stream);
+}
+
+DCONV_EXPORT const char *dconv_strerror(int status) {
+  switch (status) {
+    case DCONV_OK: return "success";
+    case DCONV_ENULL: return "a required pointer is NULL";
+    case DCONV_EINVAL: return "invalid size or variant (need C, M, K >= 1 and K <= min(Wx, Wy))";
+    case DCONV_ERANGE: return "a tensor has more than 2^31-1 elements";
+    case DCONV_EHIP: return "the HIP runtime reported an error";
+    case DCONV_EUNSUPPORTED: return "the requested kernel family cannot run this shape";
+    case DCONV_ENOMEM: return "workspace allocation failed";
+    default: return "unknown status";
+  }
+}
+
+DCONV_EXPORT int dconv_plan_single(int Wx, int Wy, int K, int M, int num_cu, dconv_plan *out) {
+  if (!out) return DCONV_ENULL;
+  const int rc = validate_sizes(1, M, Wx, Wy, K);
+  if (rc != DCONV_OK) return rc;
+  dconv::SinglePlan p;
+  dconv::plan_single(Wx, Wy, K, M, num_cu > 0 ? num_cu : 256, &p);
+  export_single(p, out);
+  return DCONV_OK;
+}
+
+DCONV_EXPORT int dconv_plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_cu,
+                                  dconv_plan *out) {
+  if (!out) return DCONV_ENULL;
+  if (variant != DCONV_VARIANT_AUTO && variant != DCONV_VARIANT_VALU &&
+      variant != DCONV_VARIANT_MFMA)
+    return DCONV_EINVAL;
+  int rc = validate_sizes(C, M, Wx, Wy, K);
+  if (rc != DCONV_OK) return rc;
+  dconv::MultiPlan p;
+  if ((rc = dconv::plan_multi(C, M, Wx, Wy, K, variant, num_cu > 0 ? num_cu : 256, &p)) !=
+      DCONV_OK)
+    return rc;
+  export_multi(p, out);
+  return DCONV_OK;
+}

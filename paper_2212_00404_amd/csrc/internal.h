@@ -1,0 +1,69 @@
+// Internal declarations shared by the host planner (api.hip) and the kernel
+// translation units.  Not part of the public interface (include/dconv.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <cstdint>
+
+#include "dconv.h"
+
+namespace dconv {
+
+// Blocks are dispatched round-robin over the 8 XCDs of an MI355X, each with
+// its own L2.  Remapping the linear block id so that consecutive ids of one
+// XCD get consecutive tiles keeps neighbouring tiles (which share halo rows
+// and filter slices) in the same L2.
+__device__ __forceinline__ int xcd_remap(int b, int n) {
+  constexpr int kXcd = 8;
+  const int per = n / kXcd;
+  const int full = per * kXcd;
+  if (b >= full) return b;
+  return (b % kXcd) * per + b / kXcd;
+}
+
+// ---------------------------------------------------------------------------
+// Single-map kernels (Eq. 2)
+// ---------------------------------------------------------------------------
+struct SinglePlan {
+  int kernel;     // 0: tiled LDS kernel for K <= kMaxTiledK, 1: generic
+  int K;
+  int rows;       // output rows per lane (R)
+  int tile_h, tile_w;
+  int tiles_x, tiles_y;
+  int m_per_block;
+  int grid;       // tiles_x * tiles_y
+  int grid_z;     // ceil(M / m_per_block)
+  int block;
+  int lds_bytes;
+};
+
+constexpr int kMaxTiledK = 11;
+
+void plan_single(int Wx, int Wy, int K, int M, int num_cu, SinglePlan *p);
+hipError_t launch_single(const SinglePlan &p, const float *I, const float *F, float *O,
+                         int Wx, int Wy, int M, hipStream_t s);
+
+// ---------------------------------------------------------------------------
+// Multi-channel kernels (Eq. 1)
+// ---------------------------------------------------------------------------
+struct MultiPlan {
+  int variant;    // DCONV_VARIANT_VALU or DCONV_VARIANT_MFMA
+  int kernel;     // instance id within the family
+  int K;
+  int tile_m;     // filters per workgroup
+  int tpy, tpx;   // output tile rows x cols per workgroup
+  int tiles_x, tiles_y;
+  int chunk_c;    // channels per LDS stage
+  int split_c;    // workgroups along the channel sum
+  int c_per_split;
+  int grid_x, grid_y, grid_z;
+  int block;
+  int lds_bytes;
+  int64_t workspace_bytes;
+};
+
+int plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_cu, MultiPlan *p);
+hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, float *O,
+                        float *ws, int C, int M, int Wx, int Wy, hipStream_t s);
+
+}  // namespace dconv

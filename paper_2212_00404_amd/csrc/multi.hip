@@ -1,0 +1,684 @@
+// Multi-channel direct convolution (paper, Section 2.1, Eq. 1; Section 3.2).
+//
+// C input maps I[C][Wy][Wx], M filters F[M][C][K][K], output O[M][Hout][Wout].
+//
+// Work division (Section 2.3 lists splitting along the filters m, along the
+// map and along the channels): a workgroup owns a tile of filters x output
+// pixels and sums over a range of channels.  Channels are consumed in stages
+// of CC channels: the filter slice F[m0:m0+MT][c0:c0+CC] (MT contiguous runs
+// of CC*K*K floats, the filter layout of Section 2.3) and the input halo tile
+// I[c0:c0+CC][y0:y0+tpy+K-1][x0:x0+tpx+K-1] are staged in LDS, then reduced
+// into register accumulators.  This is the role the paper's stride-fixed
+// blocks play (a filter segment along the channel axis plus the map lines it
+// needs), re-sized for gfx950's 160 KB LDS and 64-wide waves.
+//
+// Maps of 7x7 or 14x14 pixels give far fewer output tiles than the 256
+// compute units, so the channel sum is also split: inside a workgroup across
+// its waves (added through LDS in a fixed order), and, when that is still too
+// little work, across workgroups (partial sums to a workspace, added by a
+// second kernel in a fixed order).  The paper rejects a cross-SM channel
+// split because of the extra global traffic; on gfx950 the traffic is small
+// next to leaving most compute units idle, and it is used only when the
+// planner's estimate says so.
+//
+// Two inner products are provided:
+//   * MFMA: the stage is an implicit GEMM  acc[m][p] += A[m][k] * B[k][p]
+//     with A = filter slice and B = the im2col view of the staged input
+//     (k = channel, filter row, filter column), fed to
+//     v_mfma_f32_32x32x2_f32.  Each MFMA consumes a channel pair (c, c+1) at
+//     one (r, s): lanes 0-31 supply channel c, lanes 32-63 channel c+1.
+//   * VALU: one output pixel per lane and MR filters per wave, with the
+//     filter values wave-uniform in scalar registers and one fp32 FMA per
+//     term (packed fp32 FMAs are not used).
+#include "internal.h"
+
+namespace dconv {
+namespace {
+
+typedef float floatx16 __attribute__((ext_vector_type(16)));
+
+constexpr int kBlock = 256;
+
+// n / d for 0 <= n < 2^22 and 1 <= d < 2^11 using a float reciprocal.
+__device__ __forceinline__ int fdiv(int n, int d, float inv) {
+  int q = __float2int_rz((float)n * inv);
+  int r = n - q * d;
+  if (r >= d) { ++q; }
+  if (r < 0) { --q; }
+  return q;
+}
+
+// Stage input channels [c0, c0+CC) of rows [py0, py0+IH) and columns
+// [px0, px0+IW) into Is[cl*ICS + iy*IW + ix]; zero outside the map or past
+// c_end.  Consecutive threads take consecutive columns (coalesced rows).
+__device__ __forceinline__ void stage_input(float *__restrict__ Is, const float *__restrict__ I,
+                                            int CC, int c0, int c_end, int py0, int px0,
+                                            int IH, int IW, int ICS, int Wx, int Wy) {
+  const int per_c = IH * IW;
+  const int total = CC * per_c;
+  const float inv_pc = 1.0f / (float)per_c;
+  const float inv_iw = 1.0f / (float)IW;
+  for (int idx = threadIdx.x; idx < total; idx += kBlock) {
+    const int cl = fdiv(idx, per_c, inv_pc);
+    const int rem = idx - cl * per_c;
+    const int iy = fdiv(rem, IW, inv_iw);
+    const int ix = rem - iy * IW;
+    const int c = c0 + cl;
+    const int gy = py0 + iy;
+    const int gx = px0 + ix;
+    float v = 0.f;
+    if (c < c_end && gy < Wy && gx < Wx) v = I[((size_t)c * Wy + gy) * Wx + gx];
+    Is[cl * ICS + rem] = v;
+  }
+}
+
+struct TileArgs {
+  int C, M, Wx, Wy;
+  int tpy, tpx;       // output tile rows x cols
+  int tiles_x;        // output tiles along x
+  int ntiles;         // output tiles per map
+  int mtiles;         // filter tiles
+  int c_per_split;    // channels per workgroup along the channel sum
+  int split_c;        // workgroups along the channel sum
+  int IH, IW, ICS;    // staged input tile rows, columns, channel stride
+};
+
+// Decompose the (remapped) linear block id into output tile, filter tile and
+// channel split.  Output tiles vary fastest so that workgroups sharing a
+// filter slice run close together.
+__device__ __forceinline__ void block_coords(const TileArgs &a, int &tile, int &mt, int &split) {
+  const int nblocks = a.ntiles * a.mtiles * a.split_c;
+  int b = xcd_remap(blockIdx.x, nblocks);
+  tile = b % a.ntiles;
+  b /= a.ntiles;
+  mt = b % a.mtiles;
+  split = b / a.mtiles;
+}
+
+// ---------------------------------------------------------------------------
+// MFMA implicit-GEMM kernel
+// ---------------------------------------------------------------------------
+template <int K, int MB, int NB, int WM, int WN, int WC, int CC>
+struct MfmaCfg {
+  static constexpr int KK = K * K;
+  static constexpr int MT = 32 * MB * WM;   // filters per workgroup
+  static constexpr int PT = 32 * NB * WN;   // pixel lanes per workgroup tile
+  static constexpr int CCW = CC / WC;       // channels per wave group per stage
+  static constexpr int FROW = CC * KK;      // staged floats per filter
+  static constexpr int FP = FROW + ((FROW % 2 == 0) ? 1 : 0);  // odd pitch
+  static constexpr int F_FLOATS = MT * FP;
+  static constexpr int RED_FLOATS = (WC - 1) * WM * WN * MB * NB * 16 * 64;
+  static_assert(WM * WN * WC == 4, "four waves per workgroup");
+  static_assert(CCW % 2 == 0, "channels are consumed in pairs");
+};
+
+template <int K, int MB, int NB, int WM, int WN, int WC, int CC>
+__global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I,
+                                                     const float *__restrict__ F,
+                                                     float *__restrict__ O,
+                                                     float *__restrict__ ws, TileArgs a) {
+  using Cfg = MfmaCfg<K, MB, NB, WM, WN, WC, CC>;
+  constexpr int KK = Cfg::KK, MT = Cfg::MT, CCW = Cfg::CCW, FROW = Cfg::FROW, FP = Cfg::FP;
+  extern __shared__ float lds[];
+  float *Fs = lds;
+  float *Is = lds + Cfg::F_FLOATS;
+
+  int tile, mt, split;
+  block_coords(a, tile, mt, split);
+  const int py0 = (tile / a.tiles_x) * a.tpy;
+  const int px0 = (tile % a.tiles_x) * a.tpx;
+  const int m0 = mt * MT;
+  const int c_begin = split * a.c_per_split;
+  const int c_end = min(a.C, c_begin + a.c_per_split);
+  const int Hout = a.Wy - K + 1;
+  const int Wout = a.Wx - K + 1;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wc = wave % WC;
+  const int wmn = wave / WC;
+  const int wm = wmn % WM;
+  const int wn = wmn / WM;
+  const int col = lane & 31;
+  const int half = lane >> 5;
+
+  int a_base[MB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+    a_base[mb] = (wm * 32 * MB + mb * 32 + col) * FP + (wc * CCW + half) * KK;
+  int b_base[NB];
+  const int npix = a.tpy * a.tpx;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int p = wn * 32 * NB + nb * 32 + col;
+    int off = 0;
+    if (p < npix) {
+      const int ty = p / a.tpx;
+      off = ty * a.IW + (p - ty * a.tpx);
+    }
+    b_base[nb] = (wc * CCW + half) * a.ICS + off;
+  }
+
+  floatx16 acc[MB][NB];
+#pragma unroll
+  for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+    for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.f;
+
+  for (int c0 = c_begin; c0 < c_end; c0 += CC) {
+    // Filter slice: MT rows of CC*K*K contiguous floats each.
+    for (int idx = threadIdx.x; idx < MT * FROW; idx += kBlock) {
+      const int mrow = idx / FROW;
+      const int e = idx - mrow * FROW;
+      const int m = m0 + mrow;
+      const int c = c0 + e / KK;
+      float v = 0.f;
+      if (m < a.M && c < c_end) v = F[((size_t)m * a.C + c0) * KK + e];
+      Fs[mrow * FP + e] = v;
+    }
+    stage_input(Is, I, CC, c0, c_end, py0, px0, a.IH, a.IW, a.ICS, a.Wx, a.Wy);
+    __syncthreads();
+
+#pragma unroll
+    for (int cp = 0; cp < CCW / 2; ++cp) {
+#pragma unroll
+      for (int r = 0; r < K; ++r) {
+#pragma unroll
+        for (int s = 0; s < K; ++s) {
+          const int boff = 2 * cp * a.ICS + r * a.IW + s;
+          float av[MB], bv[NB];
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) av[mb] = Fs[a_base[mb] + 2 * cp * KK + r * K + s];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) bv[nb] = Is[b_base[nb] + boff];
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+            for (int nb = 0; nb < NB; ++nb)
+              acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[mb], bv[nb], acc[mb][nb], 0, 0, 0);
+        }
+      }
+    }
+    __syncthreads();
+  }
+
+  // Fixed-order sum of the WC channel groups through LDS.
+  if constexpr (WC > 1) {
+    float *red = lds;
+    if (wc > 0) {
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            red[((((wc - 1) * WM * WN + wmn) * MB + mb) * NB + nb) * 1024 + v * 64 + lane] =
+                acc[mb][nb][v];
+    }
+    __syncthreads();
+    if (wc != 0) return;
+#pragma unroll
+    for (int g = 1; g < WC; ++g)
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+          for (int v = 0; v < 16; ++v)
+            acc[mb][nb][v] += red[((((g - 1) * WM * WN + wmn) * MB + mb) * NB + nb) * 1024 + v * 64 + lane];
+  }
+
+  float *dst = (a.split_c == 1) ? O : ws + (size_t)split * a.M * Hout * Wout;
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb) {
+    const int p = wn * 32 * NB + nb * 32 + col;
+    if (p >= npix) continue;
+    const int ty = p / a.tpx;
+    const int gy = py0 + ty;
+    const int gx = px0 + (p - ty * a.tpx);
+    if (gy >= Hout || gx >= Wout) continue;
+    const size_t pix = (size_t)gy * Wout + gx;
+#pragma unroll
+    for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+      for (int v = 0; v < 16; ++v) {
+        const int i = 8 * (v >> 2) + 4 * half + (v & 3);
+        const int m = m0 + wm * 32 * MB + mb * 32 + i;
+        if (m < a.M) dst[(size_t)m * Hout * Wout + pix] = acc[mb][nb][v];
+      }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// VALU kernel: lane = output pixel, wave = MR filters, fp32 FMA per term
+// ---------------------------------------------------------------------------
+// KT > 0: compile-time filter size; KT == 0: any K (loops not unrolled).
+template <int KT, int MR, int WC, int CC>
+__global__ __launch_bounds__(kBlock) void multi_valu(const float *__restrict__ I,
+                                                     const float *__restrict__ F,
+                                                     float *__restrict__ O,
+                                                     float *__restrict__ ws, TileArgs a, int Krt) {
+  constexpr int CCW = CC / WC;
+  constexpr int WMV = 4 / WC;     // filter groups per workgroup
+  constexpr int MT = MR * WMV;
+  const int K = KT > 0 ? KT : Krt;
+  const int KK = K * K;
+  extern __shared__ float lds[];
+  float *Is = lds;
+
+  int tile, mt, split;
+  block_coords(a, tile, mt, split);
+  const int py0 = (tile / a.tiles_x) * a.tpy;
+  const int px0 = (tile % a.tiles_x) * a.tpx;
+  const int c_begin = split * a.c_per_split;
+  const int c_end = min(a.C, c_begin + a.c_per_split);
+  const int Hout = a.Wy - K + 1;
+  const int Wout = a.Wx - K + 1;
+
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  const int wc = wave % WC;
+  const int wm = wave / WC;
+  const int mbase = mt * MT + wm * MR;
+
+  const int npix = a.tpy * a.tpx;
+  int boff = 0;
+  if (lane < npix) {
+    const int ty = lane / a.tpx;
+    boff = ty * a.IW + (lane - ty * a.tpx);
+  }
+
+  // Filter rows read with wave-uniform addresses (scalar loads); filters past
+  // M are clamped to M-1 and their results dropped.
+  const float *Fm[MR];
+#pragma unroll
+  for (int mr = 0; mr < MR; ++mr) Fm[mr] = F + (size_t)min(mbase + mr, a.M - 1) * a.C * KK;
+
+  float acc[MR];
+#pragma unroll
+  for (int mr = 0; mr < MR; ++mr) acc[mr] = 0.f;
+
+  for (int c0 = c_begin; c0 < c_end; c0 += CC) {
+    stage_input(Is, I, CC, c0, c_end, py0, px0, a.IH, a.IW, a.ICS, a.Wx, a.Wy);
+    __syncthreads();
+    for (int cl = wc * CCW; cl < (wc + 1) * CCW; ++cl) {
+      const int c = min(c0 + cl, a.C - 1);  // staged input is zero past c_end
+      const float *Ic = Is + cl * a.ICS + boff;
+      if constexpr (KT > 0) {
+#pragma unroll
+        for (int r = 0; r < KT; ++r) {
+          float f[MR][KT];
+#pragma unroll
+          for (int mr = 0; mr < MR; ++mr)
+#pragma unroll
+            for (int s = 0; s < KT; ++s) f[mr][s] = Fm[mr][(size_t)c * KK + r * KT + s];
+#pragma unroll
+          for (int s = 0; s < KT; ++s) {
+            const float v = Ic[r * a.IW + s];
+#pragma unroll
+            for (int mr = 0; mr < MR; ++mr) acc[mr] = __builtin_fmaf(v, f[mr][s], acc[mr]);
+          }
+        }
+      } else {
+        for (int r = 0; r < K; ++r)
+          for (int s = 0; s < K; ++s) {
+            const float v = Ic[r * a.IW + s];
+#pragma unroll
+            for (int mr = 0; mr < MR; ++mr)
+              acc[mr] = __builtin_fmaf(v, Fm[mr][(size_t)c * KK + r * K + s], acc[mr]);
+          }
+      }
+    }
+    __syncthreads();
+  }
+
+  if constexpr (WC > 1) {
+    float *red = lds;
+    if (wc > 0) {
+#pragma unroll
+      for (int mr = 0; mr < MR; ++mr) red[(((wc - 1) * WMV + wm) * MR + mr) * 64 + lane] = acc[mr];
+    }
+    __syncthreads();
+    if (wc != 0) return;
+#pragma unroll
+    for (int g = 1; g < WC; ++g)
+#pragma unroll
+      for (int mr = 0; mr < MR; ++mr) acc[mr] += red[(((g - 1) * WMV + wm) * MR + mr) * 64 + lane];
+  }
+
+  if (lane >= npix) return;
+  const int ty = lane / a.tpx;
+  const int gy = py0 + ty;
+  const int gx = px0 + (lane - ty * a.tpx);
+  if (gy >= Hout || gx >= Wout) return;
+  float *dst = (a.split_c == 1) ? O : ws + (size_t)split * a.M * Hout * Wout;
+  const size_t pix = (size_t)gy * Wout + gx;
+#pragma unroll
+  for (int mr = 0; mr < MR; ++mr)
+    if (mbase + mr < a.M) dst[(size_t)(mbase + mr) * Hout * Wout + pix] = acc[mr];
+}
+
+// Any size: one output per thread, operands read through the caches.  Used
+// when no tiled kernel's LDS footprint fits (very large filters).
+__global__ __launch_bounds__(256) void multi_generic(const float *__restrict__ I,
+                                                     const float *__restrict__ F,
+                                                     float *__restrict__ O, int C, int M, int Wx,
+                                                     int Wy, int K) {
+  const int Hout = Wy - K + 1;
+  const int Wout = Wx - K + 1;
+  const int64_t total = (int64_t)M * Hout * Wout;
+  const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (idx >= total) return;
+  const int x = (int)(idx % Wout);
+  const int64_t my = idx / Wout;
+  const int y = (int)(my % Hout);
+  const int m = (int)(my / Hout);
+  float acc = 0.f;
+  for (int c = 0; c < C; ++c) {
+    const float *Fc = F + ((int64_t)m * C + c) * K * K;
+    for (int r = 0; r < K; ++r) {
+      const float *irow = I + ((int64_t)c * Wy + y + r) * Wx + x;
+      for (int s = 0; s < K; ++s) acc = __builtin_fmaf(irow[s], Fc[r * K + s], acc);
+    }
+  }
+  O[idx] = acc;
+}
+
+// O[i] = sum_{s < S} ws[s][i], added in the order s = 0, 1, ..., S-1.
+__global__ __launch_bounds__(256) void split_sum(const float *__restrict__ ws,
+                                                 float *__restrict__ O, int64_t n, int S) {
+  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+  if (i >= n) return;
+  float acc = ws[i];
+  for (int s = 1; s < S; ++s) acc += ws[(int64_t)s * n + i];
+  O[i] = acc;
+}
+
+// Dynamic LDS per workgroup the planner may request (gfx950: 160 KB per CU).
+constexpr int kMaxLds = 160 * 1024;
+
+// Kernels are allowed the full LDS once per instance, before their first
+// launch (thread-safe static initialisation).
+template <typename Kern>
+hipError_t allow_full_lds(Kern kern) {
+  static const hipError_t e = hipFuncSetAttribute(
+      reinterpret_cast<const void *>(kern), hipFuncAttributeMaxDynamicSharedMemorySize, kMaxLds);
+  return e;
+}
+
+// ---------------------------------------------------------------------------
+// Kernel table
+// ---------------------------------------------------------------------------
+// Each family has a few workgroup shapes; the planner picks one per call.
+struct MfmaShape { int MB, NB, WM, WN, WC, CC; };
+constexpr MfmaShape kMfmaShapes[] = {
+    {1, 2, 1, 1, 4, 16},  // 32 filters x 64 pixels, channel sum split over 4 waves
+    {1, 1, 2, 2, 1, 8},   // 64 x 64
+    {1, 2, 2, 2, 1, 8},   // 64 x 128
+    {2, 2, 2, 2, 1, 8},   // 128 x 128
+};
+constexpr int kNumMfma = sizeof(kMfmaShapes) / sizeof(kMfmaShapes[0]);
+
+struct ValuShape { int MR, WC, CC; };
+constexpr ValuShape kValuShapes[] = {
+    {8, 4, 16},  // 8 filters x 64 pixels, channel sum split over 4 waves
+    {8, 1, 8},   // 32 filters x 64 pixels
+};
+constexpr int kNumValu = sizeof(kValuShapes) / sizeof(kValuShapes[0]);
+
+template <int K, int S>
+hipError_t launch_mfma_shape(const MultiPlan &p, const float *I, const float *F, float *O,
+                             float *ws, const TileArgs &a, hipStream_t st) {
+  constexpr MfmaShape sh = kMfmaShapes[S];
+  auto kern = multi_mfma<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC, sh.CC>;
+  if (hipError_t e = allow_full_lds(kern); e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(kBlock), p.lds_bytes, st, I, F, O, ws, a);
+  return hipGetLastError();
+}
+
+template <int K>
+hipError_t launch_mfma_k(const MultiPlan &p, const float *I, const float *F, float *O,
+                         float *ws, const TileArgs &a, hipStream_t st) {
+  switch (p.kernel) {
+    case 0: return launch_mfma_shape<K, 0>(p, I, F, O, ws, a, st);
+    case 1: return launch_mfma_shape<K, 1>(p, I, F, O, ws, a, st);
+    case 2: return launch_mfma_shape<K, 2>(p, I, F, O, ws, a, st);
+    case 3: return launch_mfma_shape<K, 3>(p, I, F, O, ws, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+template <int KT, int S>
+hipError_t launch_valu_shape(const MultiPlan &p, const float *I, const float *F, float *O,
+                             float *ws, const TileArgs &a, hipStream_t st) {
+  constexpr ValuShape sh = kValuShapes[S];
+  auto kern = multi_valu<KT, sh.MR, sh.WC, sh.CC>;
+  if (hipError_t e = allow_full_lds(kern); e != hipSuccess) return e;
+  hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(kBlock), p.lds_bytes, st, I, F, O, ws, a, p.K);
+  return hipGetLastError();
+}
+
+template <int KT>
+hipError_t launch_valu_k(const MultiPlan &p, const float *I, const float *F, float *O,
+                         float *ws, const TileArgs &a, hipStream_t st) {
+  switch (p.kernel) {
+    case 0: return launch_valu_shape<KT, 0>(p, I, F, O, ws, a, st);
+    case 1: return launch_valu_shape<KT, 1>(p, I, F, O, ws, a, st);
+    default: return hipErrorInvalidValue;
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Planner
+// ---------------------------------------------------------------------------
+constexpr int kMfmaMaxK = 7;
+constexpr int kGenericKernel = 99;
+
+struct TileChoice { int tpy, tpx, tiles_x, tiles_y; int64_t lanes; };
+
+// Rectangular output tiles of at most `cap` pixels; pick the shape that
+// wastes the fewest pixel lanes over the whole map (ties: wider tiles, for
+// coalesced rows).
+TileChoice choose_tile(int Hout, int Wout, int cap) {
+  TileChoice best{1, 1, Wout, Hout, INT64_MAX};
+  for (int tpx = 1; tpx <= cap && tpx <= Wout; ++tpx) {
+    int tpy = cap / tpx;
+    if (tpy > Hout) tpy = Hout;
+    if (tpy < 1) continue;
+    const int tx = (Wout + tpx - 1) / tpx;
+    const int ty = (Hout + tpy - 1) / tpy;
+    const int64_t lanes = (int64_t)tx * ty * cap;
+    if (lanes < best.lanes || (lanes == best.lanes && tpx > best.tpx))
+      best = TileChoice{tpy, tpx, tx, ty, lanes};
+  }
+  return best;
+}
+
+struct Candidate {
+  int kernel, MT, PT, WC, CC, mfma_per_kstep;  // per wave per (channel pair, r, s)
+  int f_floats_fixed;  // LDS floats for the filter slice (MFMA), 0 for VALU
+  int red_floats;
+};
+
+Candidate mfma_candidate(int i, int K) {
+  const MfmaShape s = kMfmaShapes[i];
+  const int KK = K * K;
+  const int frow = s.CC * KK;
+  const int fp = frow + ((frow % 2 == 0) ? 1 : 0);
+  const int MT = 32 * s.MB * s.WM;
+  return Candidate{i, MT, 32 * s.NB * s.WN, s.WC, s.CC, s.MB * s.NB, MT * fp,
+                   (s.WC - 1) * s.WM * s.WN * s.MB * s.NB * 16 * 64};
+}
+
+Candidate valu_candidate(int i) {
+  const ValuShape s = kValuShapes[i];
+  return Candidate{i, s.MR * (4 / s.WC), 64, s.WC, s.CC, s.MR, 0, (s.WC - 1) * (4 / s.WC) * s.MR * 64};
+}
+
+// Rough time model in GPU clock cycles, used only to rank candidates.
+//   compute: per-wave inner-product cycles of the busiest compute unit
+//   staging: one exposed load latency per stage
+//   split:   partial sums written, re-read and summed by a second launch
+double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, int Wout,
+                int num_cu, const TileChoice &t, int split, int cps) {
+  const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
+  const int64_t mtiles = (M + cd.MT - 1) / cd.MT;
+  const int64_t blocks = ntiles * mtiles * split;
+  const int stages = (cps + cd.CC - 1) / cd.CC;
+  const int kk = K * K;
+  // cycles of one wave per stage: MFMA 32x32x2 f32 = 64 cycles (2 channels);
+  // VALU fp32 FMA on 64 lanes = 4 cycles per filter value.
+  const double per_stage = mfma ? (double)(cd.CC / cd.WC / 2) * kk * cd.mfma_per_kstep * 64.0
+                                : (double)(cd.CC / cd.WC) * kk * cd.mfma_per_kstep * 4.0;
+  const int64_t waves_per_cu = (blocks + num_cu - 1) / num_cu;  // 1 wave per SIMD per block
+  const double compute = (double)waves_per_cu * stages * per_stage;
+  const double staging = (double)stages * 2500.0;
+  double extra = 0.0;
+  if (split > 1) {
+    const double bytes = 2.0 * split * (double)M * Hout * Wout * 4.0;
+    extra = 6000.0 + bytes / 2000.0;  // ~5 TB/s at 2.4 GHz ~ 2 KB per cycle
+  }
+  return compute + staging + extra;
+}
+
+int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, MultiPlan *best) {
+  const int Hout = Wy - K + 1, Wout = Wx - K + 1;
+  double best_t = 1e300;
+  const int n = mfma ? kNumMfma : kNumValu;
+  bool found = false;
+  for (int i = 0; i < n; ++i) {
+    const Candidate cd = mfma ? mfma_candidate(i, K) : valu_candidate(i);
+    const TileChoice t = choose_tile(Hout, Wout, cd.PT);
+    const int IH = t.tpy + K - 1, IW = t.tpx + K - 1;
+    int ICS = IH * IW;
+    const int64_t lds_f = (int64_t)cd.f_floats_fixed + (int64_t)cd.CC * ICS;
+    const int64_t lds_floats = lds_f > cd.red_floats ? lds_f : cd.red_floats;
+    if (lds_floats * 4 > kMaxLds) continue;
+    for (int split = 1; split <= 64; split *= 2) {
+      // channels per split: a multiple of the stage size
+      int cps = (C + split - 1) / split;
+      cps = (cps + cd.CC - 1) / cd.CC * cd.CC;
+      const int real_split = (C + cps - 1) / cps;
+      if (real_split != split) break;
+      const double tm = estimate(cd, mfma, C, M, K, Hout, Wout, num_cu, t, split, cps);
+      if (tm < best_t) {
+        best_t = tm;
+        found = true;
+        MultiPlan p{};
+        p.variant = mfma ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
+        p.kernel = i;
+        p.K = K;
+        p.tile_m = cd.MT;
+        p.tpy = t.tpy;
+        p.tpx = t.tpx;
+        p.tiles_x = t.tiles_x;
+        p.tiles_y = t.tiles_y;
+        p.chunk_c = cd.CC;
+        p.split_c = split;
+        p.c_per_split = cps;
+        p.grid_x = (int)((int64_t)t.tiles_x * t.tiles_y * ((M + cd.MT - 1) / cd.MT) * split);
+        p.grid_y = 1;
+        p.grid_z = 1;
+        p.block = kBlock;
+        p.lds_bytes = (int)(lds_floats * 4);
+        p.workspace_bytes = split > 1 ? (int64_t)split * M * Hout * Wout * 4 : 0;
+        *best = p;
+      }
+    }
+  }
+  if (!found && !mfma) {
+    // No tiled shape fits in LDS: one output per thread from the caches.
+    const int64_t total = (int64_t)M * Hout * Wout;
+    MultiPlan p{};
+    p.variant = DCONV_VARIANT_VALU;
+    p.kernel = kGenericKernel;
+    p.K = K;
+    p.tile_m = 1;
+    p.tpy = 1;
+    p.tpx = 1;
+    p.tiles_x = Wout;
+    p.tiles_y = Hout;
+    p.chunk_c = C;
+    p.split_c = 1;
+    p.c_per_split = C;
+    p.grid_x = (int)((total + 255) / 256);
+    p.grid_y = p.grid_z = 1;
+    p.block = 256;
+    p.lds_bytes = 0;
+    p.workspace_bytes = 0;
+    *best = p;
+    found = true;
+  }
+  return found ? DCONV_OK : DCONV_EUNSUPPORTED;
+}
+
+}  // namespace
+
+int plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_cu, MultiPlan *p) {
+  if (num_cu <= 0) num_cu = 256;
+  if (variant == DCONV_VARIANT_MFMA) {
+    if (K > kMfmaMaxK) return DCONV_EUNSUPPORTED;
+    return plan_family(C, M, Wx, Wy, K, true, num_cu, p);
+  }
+  if (variant == DCONV_VARIANT_VALU) return plan_family(C, M, Wx, Wy, K, false, num_cu, p);
+  // Automatic: the matrix cores deliver twice the fp32 rate of unpacked
+  // vector FMAs, so they are preferred wherever a kernel exists.
+  if (K <= kMfmaMaxK && plan_family(C, M, Wx, Wy, K, true, num_cu, p) == DCONV_OK) return DCONV_OK;
+  return plan_family(C, M, Wx, Wy, K, false, num_cu, p);
+}
+
+hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, float *O, float *ws,
+                        int C, int M, int Wx, int Wy, hipStream_t st) {
+  TileArgs a{};
+  a.C = C;
+  a.M = M;
+  a.Wx = Wx;
+  a.Wy = Wy;
+  a.tpy = p.tpy;
+  a.tpx = p.tpx;
+  a.tiles_x = p.tiles_x;
+  a.ntiles = p.tiles_x * p.tiles_y;
+  a.mtiles = (M + p.tile_m - 1) / p.tile_m;
+  a.c_per_split = p.c_per_split;
+  a.split_c = p.split_c;
+  a.IH = p.tpy + p.K - 1;
+  a.IW = p.tpx + p.K - 1;
+  a.ICS = a.IH * a.IW;
+  hipError_t e;
+  if (p.kernel == kGenericKernel) {
+    hipLaunchKernelGGL(multi_generic, dim3(p.grid_x), dim3(256), 0, st, I, F, O, C, M, Wx, Wy, p.K);
+    return hipGetLastError();
+  }
+  if (p.variant == DCONV_VARIANT_MFMA) {
+    switch (p.K) {
+      case 1: e = launch_mfma_k<1>(p, I, F, O, ws, a, st); break;
+      case 2: e = launch_mfma_k<2>(p, I, F, O, ws, a, st); break;
+      case 3: e = launch_mfma_k<3>(p, I, F, O, ws, a, st); break;
+      case 4: e = launch_mfma_k<4>(p, I, F, O, ws, a, st); break;
+      case 5: e = launch_mfma_k<5>(p, I, F, O, ws, a, st); break;
+      case 6: e = launch_mfma_k<6>(p, I, F, O, ws, a, st); break;
+      case 7: e = launch_mfma_k<7>(p, I, F, O, ws, a, st); break;
+      default: return hipErrorInvalidValue;
+    }
+  } else {
+    switch (p.K) {
+      case 1: e = launch_valu_k<1>(p, I, F, O, ws, a, st); break;
+      case 2: e = launch_valu_k<2>(p, I, F, O, ws, a, st); break;
+      case 3: e = launch_valu_k<3>(p, I, F, O, ws, a, st); break;
+      case 4: e = launch_valu_k<4>(p, I, F, O, ws, a, st); break;
+      case 5: e = launch_valu_k<5>(p, I, F, O, ws, a, st); break;
+      case 6: e = launch_valu_k<6>(p, I, F, O, ws, a, st); break;
+      case 7: e = launch_valu_k<7>(p, I, F, O, ws, a, st); break;
+      default: e = launch_valu_k<0>(p, I, F, O, ws, a, st); break;
+    }
+  }
+  if (e != hipSuccess || p.split_c == 1) return e;
+  const int64_t n = (int64_t)M * (Wy - p.K + 1) * (Wx - p.K + 1);
+  hipLaunchKernelGGL(split_sum, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, ws, O, n,
+                     p.split_c);
+  return hipGetLastError();
+}
+
+}  // namespace dconv

@@ -1,0 +1,174 @@
+"""The C ABI without a GPU: the library loads, exports what include/dconv.h
+declares, validates arguments before any HIP call, and plans launches whose
+grids cover every output and fit the gfx950 limits (host logic only)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2212_00404_amd as dc
+from dconv_workloads import WORKLOADS
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "dconv.h")
+LDS_MAX = 160 * 1024
+
+# non-NULL placeholders: validation rejects before anything is dereferenced
+P = ctypes.c_void_p(0x1000)
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(dconv_\w+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_function():
+    lib = dc.load()
+    names = declared_functions()
+    assert set(names) == set(dc.EXPORTED), names
+    for name in names:
+        assert hasattr(lib, name), name
+
+
+def test_only_api_symbols_are_exported():
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--defined-only", dc.dconv.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    text_syms = [l.split()[-1] for l in out.splitlines() if " T " in l]
+    assert sorted(text_syms) == sorted(dc.EXPORTED)
+
+
+def test_null_pointers():
+    lib = dc.load()
+    assert lib.dconv_single(None, P, P, 8, 8, 3, 1, None) == dc.dconv.ENULL
+    assert lib.dconv_single(P, None, P, 8, 8, 3, 1, None) == dc.dconv.ENULL
+    assert lib.dconv_single(P, P, None, 8, 8, 3, 1, None) == dc.dconv.ENULL
+    assert lib.dconv_multi(None, P, P, 2, 2, 8, 8, 3, None) == dc.dconv.ENULL
+    assert lib.dconv_multi_variant(P, P, None, 2, 2, 8, 8, 3, 0, None) == dc.dconv.ENULL
+
+
+@pytest.mark.parametrize("args", [
+    (8, 8, 0, 1),     # K < 1
+    (8, 8, 9, 1),     # K > Wx
+    (9, 4, 5, 1),     # K > Wy (argument order Wx, Wy, K, M)
+    (8, 8, 3, 0),     # M < 1
+    (0, 8, 1, 1),     # Wx < 1
+])
+def test_single_invalid_sizes(args):
+    Wx, Wy, K, M = args
+    assert dc.load().dconv_single(P, P, P, Wx, Wy, K, M, None) == dc.dconv.EINVAL
+
+
+@pytest.mark.parametrize("args", [
+    (0, 2, 8, 8, 3),   # C < 1
+    (2, 0, 8, 8, 3),   # M < 1
+    (2, 2, 8, 8, 0),   # K < 1
+    (2, 2, 4, 9, 5),   # K > Wx (order C, M, Wx, Wy, K)
+    (2, 2, 9, 4, 5),   # K > Wy
+])
+def test_multi_invalid_sizes(args):
+    C, M, Wx, Wy, K = args
+    assert dc.load().dconv_multi(P, P, P, C, M, Wx, Wy, K, None) == dc.dconv.EINVAL
+
+
+def test_bad_variant():
+    assert dc.load().dconv_multi_variant(P, P, P, 2, 2, 8, 8, 3, 7, None) == dc.dconv.EINVAL
+
+
+def test_range_limits():
+    lib = dc.load()
+    # input 65536 x 65536 = 2^32 elements
+    assert lib.dconv_single(P, P, P, 65536, 65536, 3, 1, None) == dc.dconv.ERANGE
+    # filters: M*C*K*K = 2^31
+    assert lib.dconv_multi(P, P, P, 65536, 32768, 1, 1, 1, None) == dc.dconv.ERANGE
+    # output M*Hout*Wout > 2^31-1
+    assert lib.dconv_single(P, P, P, 40000, 40000, 1, 2, None) == dc.dconv.ERANGE
+
+
+def test_strerror():
+    for code in (0, -1, -2, -3, -4, -5, -6):
+        assert dc.strerror(code) and dc.strerror(code) != "unknown status"
+    assert dc.strerror(12345) == "unknown status"
+
+
+def _check_single_plan(Wx, Wy, K, M):
+    p = dc.plan_single(Wx, Wy, K, M)
+    Hout, Wout = Wy - K + 1, Wx - K + 1
+    assert p["lds_bytes"] <= LDS_MAX
+    assert p["block"] in (64, 128, 256, 512, 1024)
+    if p["kernel"] == 0:
+        tiles_x = -(-Wout // p["tile_w"])
+        tiles_y = -(-Hout // p["tile_h"])
+        assert p["grid_x"] == tiles_x * tiles_y
+        assert p["grid_y"] * p["tile_m"] >= M
+        assert (p["grid_y"] - 1) * p["tile_m"] < M
+    else:
+        assert p["grid_x"] * p["block"] >= M * Hout * Wout
+    return p
+
+
+def _check_multi_plan(C, M, Wx, Wy, K, variant="auto"):
+    p = dc.plan_multi(C, M, Wx, Wy, K, variant)
+    Hout, Wout = Wy - K + 1, Wx - K + 1
+    assert p["lds_bytes"] <= LDS_MAX
+    if p["kernel"] == 99:   # one output per thread
+        assert p["grid_x"] * p["block"] >= M * Hout * Wout
+        return p
+    tiles = -(-Hout // p["tile_h"]) * -(-Wout // p["tile_w"])
+    mtiles = -(-M // p["tile_m"])
+    assert p["grid_x"] == tiles * mtiles * p["split_c"]
+    cps = -(-C // p["split_c"])
+    assert cps <= C or p["split_c"] == 1
+    assert p["workspace_bytes"] == (p["split_c"] * M * Hout * Wout * 4 if p["split_c"] > 1 else 0)
+    if variant == "mfma":
+        assert p["variant"] == dc.dconv.VARIANT_MFMA
+        assert p["tile_h"] * p["tile_w"] <= 128
+    if variant == "valu":
+        assert p["variant"] == dc.dconv.VARIANT_VALU
+    return p
+
+
+@pytest.mark.parametrize("name", sorted(WORKLOADS))
+def test_plans_for_workloads(name):
+    w = WORKLOADS[name]
+    if w.kind == "single":
+        p = _check_single_plan(w.Wx, w.Wy, w.K, w.M)
+        # enough workgroups to occupy 256 compute units at the large size
+        if w.Wx >= 1024:
+            assert p["grid_x"] * p["grid_y"] >= 256
+    else:
+        for v in ("auto", "valu", "mfma"):
+            _check_multi_plan(w.C, w.M, w.Wx, w.Wy, w.K, v)
+        p = dc.plan_multi(w.C, w.M, w.Wx, w.Wy, w.K)
+        assert p["variant"] == dc.dconv.VARIANT_MFMA
+
+
+@pytest.mark.parametrize("shape", [
+    (1, 1, 1, 1), (5, 7, 3, 2), (300, 17, 5, 3), (64, 64, 11, 1), (100, 80, 13, 2),
+    (4096, 4096, 11, 1), (28, 28, 5, 512), (1024, 1024, 3, 32), (37, 1000, 9, 4)])
+def test_single_plan_shapes(shape):
+    _check_single_plan(*shape)
+
+
+@pytest.mark.parametrize("shape", [
+    (1, 1, 1, 1, 1), (3, 5, 9, 7, 3), (512, 512, 9, 9, 3), (7, 33, 40, 23, 5), (2, 3, 20, 20, 9),
+    (16, 16, 64, 64, 31), (64, 130, 57, 31, 7), (3, 64, 224, 224, 7), (1, 1, 4096, 2, 2)])
+def test_multi_plan_shapes(shape):
+    C, M, Wx, Wy, K = shape
+    for v in ("auto", "valu") + (("mfma",) if K <= 7 else ()):
+        _check_multi_plan(C, M, Wx, Wy, K, v)
+
+
+def test_mfma_refuses_large_filters():
+    with pytest.raises(RuntimeError):
+        dc.plan_multi(4, 4, 20, 20, 9, "mfma")
+
+
+def test_small_maps_split_the_channel_sum():
+    """7x7 outputs with 512 channels give far fewer tiles than compute units:
+    the planner must split the channel sum across workgroups."""
+    p = dc.plan_multi(512, 512, 9, 9, 3)
+    assert p["split_c"] > 1
+    assert p["grid_x"] >= 256

@@ -1,0 +1,143 @@
+"""GPU parity: libdconv through its C ABI against the fp64 CPU oracle.
+
+Bar: integer-valued inputs (every partial sum exact in fp32) are bit-exact;
+floating-point inputs satisfy |O - O64| <= 1e-5 * sum|I*F| per output.
+Every workload runs at full size, for both kernel families on multi-channel
+shapes, and a set of ragged and degenerate shapes covers tile tails,
+misaligned rows, odd channel counts and the fallback kernels.
+"""
+import numpy as np
+import pytest
+import torch
+
+import paper_2212_00404_amd as dc
+from dconv_workloads import WORKLOADS, make, random_arrays
+from gpu_util import (assert_exact, assert_within, gpu_multi, gpu_single, oracle_multi,
+                      oracle_single)
+
+pytestmark = pytest.mark.gpu
+
+SINGLE = sorted(n for n, w in WORKLOADS.items() if w.kind == "single")
+MULTI = sorted(n for n, w in WORKLOADS.items() if w.kind == "multi")
+
+
+@pytest.mark.parametrize("name", SINGLE)
+@pytest.mark.parametrize("variant", ["float", "int"])
+def test_single_workload(name, variant):
+    I, F = make(name, variant)
+    O = gpu_single(I, F)
+    O64, A64 = oracle_single(I, F)
+    if variant == "int":
+        assert_exact(O, O64, name)
+    else:
+        assert_within(O, O64, A64, name)
+
+
+@pytest.mark.parametrize("name", MULTI)
+@pytest.mark.parametrize("family", ["auto", "mfma", "valu"])
+@pytest.mark.parametrize("variant", ["float", "int"])
+def test_multi_workload(name, family, variant):
+    I, F = make(name, variant)
+    O = gpu_multi(I, F, family)
+    O64, A64 = oracle_multi(I, F)
+    if variant == "int":
+        assert_exact(O, O64, "%s/%s" % (name, family))
+    else:
+        assert_within(O, O64, A64, "%s/%s" % (name, family))
+
+
+# (Wx, Wy, K, M): tails in both directions, Wx % 4 != 0 (unaligned rows), K up
+# to the generic kernel (K > 11), one output, one pixel, several filters.
+SINGLE_SHAPES = [
+    (1, 1, 1, 1), (5, 5, 5, 2), (7, 3, 3, 1), (300, 17, 5, 3), (257, 33, 3, 1),
+    (258, 70, 2, 4), (520, 65, 7, 2), (61, 200, 9, 1), (130, 45, 11, 3), (100, 80, 13, 2),
+    (64, 64, 16, 1), (33, 40, 1, 5), (1030, 9, 4, 1), (96, 96, 6, 37), (80, 81, 8, 1),
+    (90, 91, 10, 2),
+]
+
+
+@pytest.mark.parametrize("shape", SINGLE_SHAPES, ids=[str(s) for s in SINGLE_SHAPES])
+def test_single_shapes(shape):
+    Wx, Wy, K, M = shape
+    I, F = random_arrays(1, M, Wx, Wy, K, seed=sum(shape) * 7919)
+    O64, A64 = oracle_single(I[0], F[:, 0])
+    assert_within(gpu_single(I[0], F[:, 0]), O64, A64, "single %r" % (shape,))
+    Ii, Fi = random_arrays(1, M, Wx, Wy, K, seed=sum(shape) * 7919 + 1, variant="int")
+    O64i, _ = oracle_single(Ii[0], Fi[:, 0])
+    assert_exact(gpu_single(Ii[0], Fi[:, 0]), O64i, "single int %r" % (shape,))
+
+
+# (C, M, Wx, Wy, K): odd channel counts (the MFMA path pairs channels), M not a
+# multiple of any filter tile, K from 1 to beyond the MFMA kernels, tiny and
+# non-square maps, and a filter too large for any LDS tile.
+MULTI_SHAPES = [
+    (1, 1, 1, 1, 1), (3, 5, 9, 7, 3), (5, 33, 12, 12, 1), (7, 40, 10, 13, 2), (2, 3, 20, 20, 4),
+    (17, 70, 23, 19, 5), (9, 31, 16, 30, 6), (4, 65, 25, 25, 7), (6, 9, 20, 20, 9),
+    (3, 4, 17, 21, 11), (2, 3, 40, 40, 31), (33, 129, 15, 15, 3), (64, 64, 7, 7, 7),
+    (3, 64, 70, 70, 7), (130, 7, 9, 9, 3), (1, 96, 100, 3, 3),
+]
+
+
+@pytest.mark.parametrize("shape", MULTI_SHAPES, ids=[str(s) for s in MULTI_SHAPES])
+def test_multi_shapes(shape):
+    C, M, Wx, Wy, K = shape
+    families = ["auto", "valu"] + (["mfma"] if K <= 7 else [])
+    I, F = random_arrays(C, M, Wx, Wy, K, seed=sum(shape) * 104729)
+    O64, A64 = oracle_multi(I, F)
+    Ii, Fi = random_arrays(C, M, Wx, Wy, K, seed=sum(shape) * 104729 + 1, variant="int")
+    O64i, _ = oracle_multi(Ii, Fi)
+    for fam in families:
+        assert_within(gpu_multi(I, F, fam), O64, A64, "multi %r %s" % (shape, fam))
+        assert_exact(gpu_multi(Ii, Fi, fam), O64i, "multi int %r %s" % (shape, fam))
+
+
+def test_delta_filter_is_bit_exact_on_random_floats():
+    """A one-hot filter copies the shifted input exactly (x * 1 + 0 is exact)."""
+    rng = np.random.default_rng(5)
+    I = rng.uniform(-1, 1, (3, 40, 50)).astype(np.float32)
+    F = np.zeros((4, 3, 5, 5), np.float32)
+    picks = [(0, 1, 3), (2, 4, 0), (1, 0, 2), (2, 3, 4)]
+    for m, (c, r, s) in enumerate(picks):
+        F[m, c, r, s] = 1.0
+    for fam in ("mfma", "valu"):
+        O = gpu_multi(I, F, fam)
+        for m, (c, r, s) in enumerate(picks):
+            assert np.array_equal(O[m], I[c, r:r + 36, s:s + 46]), fam
+    Fs = np.zeros((2, 7, 7), np.float32)
+    Fs[0, 2, 5] = 1.0
+    Fs[1, 6, 0] = 1.0
+    O = gpu_single(I[0], Fs)
+    assert np.array_equal(O[0], I[0, 2:36, 5:49])
+    assert np.array_equal(O[1], I[0, 6:40, 0:44])
+
+
+@pytest.mark.parametrize("name", ["multi_c512_9x9_m512_k3", "single_64x64_m1_k3"])
+def test_repeated_calls_are_bitwise_identical(name):
+    """Fixed summation order (including the cross-workgroup channel split)."""
+    I, F = make(name)
+    run = gpu_single if WORKLOADS[name].kind == "single" else gpu_multi
+    first = run(I, F)
+    for _ in range(5):
+        assert np.array_equal(run(I, F), first)
+
+
+def test_every_output_written_on_a_side_stream():
+    """Output buffer pre-filled with NaN, work enqueued on a non-default stream."""
+    I, F = make("multi_c256_28x28_m256_k1")
+    It = torch.from_numpy(I).cuda()
+    Ft = torch.from_numpy(F).cuda()
+    out = torch.full((256, 28, 28), float("nan"), device="cuda")
+    s = torch.cuda.Stream()
+    torch.cuda.synchronize()
+    with torch.cuda.stream(s):
+        dc.multi(It, Ft, out=out)
+    s.synchronize()
+    O64, A64 = oracle_multi(I, F)
+    assert_within(out.cpu().numpy(), O64, A64, "side stream")
+    Is, Fs = make("single_64x64_m1_k3")
+    outs = torch.full((1, 62, 62), float("nan"), device="cuda")
+    with torch.cuda.stream(s):
+        dc.single(torch.from_numpy(Is).cuda(), torch.from_numpy(Fs).cuda(), out=outs)
+    s.synchronize()
+    O64, A64 = oracle_single(Is, Fs)
+    assert_within(outs.cpu().numpy(), O64, A64, "side stream single")
