@@ -40,7 +40,27 @@ def parse():
                     help="kernel family for multi-channel workloads")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-reps", type=int, default=2)
+    ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
+                    help="instead of convolving, copy a MIB-sized device buffer --steps "
+                         "times (reference kernel for scaling HBM byte counters)")
     return ap.parse_args()
+
+
+def copy_probe(mib, steps):
+    """A plain device-to-device copy of known size: its FETCH_SIZE/WRITE_SIZE
+    counters per dispatch calibrate the counters of the convolution kernels."""
+    import torch
+    n = mib * (1 << 20) // 4
+    src = torch.rand(n, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(steps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    dt = (time.perf_counter() - t0) / steps
+    print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4,
+                      "steps": steps, "gbs": round(2 * n * 4 / dt / 1e9, 1)}), flush=True)
 
 
 def traffic_for(kernel_tag):
@@ -89,6 +109,10 @@ def main():
         print("bench.py measures one GPU: this build has no multi-GPU path "
               "(run with --gpus 1)", file=sys.stderr)
         sys.exit(2)
+
+    if args.copy_probe:
+        copy_probe(args.copy_probe, args.steps)
+        return
 
     import torch
     import paper_2212_00404_amd as dc

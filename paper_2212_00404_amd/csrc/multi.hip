@@ -50,25 +50,40 @@ __device__ __forceinline__ int fdiv(int n, int d, float inv) {
 
 // Stage input channels [c0, c0+CC) of rows [py0, py0+IH) and columns
 // [px0, px0+IW) into Is[cl*ICS + iy*IW + ix]; zero outside the map or past
-// c_end.  Consecutive threads take consecutive columns (coalesced rows).
+// c_end.  Consecutive threads take consecutive columns (coalesced rows), and
+// each thread issues kBatch loads before its first LDS write so that they
+// are in flight together.
 __device__ __forceinline__ void stage_input(float *__restrict__ Is, const float *__restrict__ I,
                                             int CC, int c0, int c_end, int py0, int px0,
                                             int IH, int IW, int ICS, int Wx, int Wy) {
+  constexpr int kBatch = 8;
   const int per_c = IH * IW;
   const int total = CC * per_c;
   const float inv_pc = 1.0f / (float)per_c;
   const float inv_iw = 1.0f / (float)IW;
-  for (int idx = threadIdx.x; idx < total; idx += kBlock) {
-    const int cl = fdiv(idx, per_c, inv_pc);
-    const int rem = idx - cl * per_c;
-    const int iy = fdiv(rem, IW, inv_iw);
-    const int ix = rem - iy * IW;
-    const int c = c0 + cl;
-    const int gy = py0 + iy;
-    const int gx = px0 + ix;
-    float v = 0.f;
-    if (c < c_end && gy < Wy && gx < Wx) v = I[((size_t)c * Wy + gy) * Wx + gx];
-    Is[cl * ICS + rem] = v;
+  for (int base = threadIdx.x; base < total; base += kBlock * kBatch) {
+    float v[kBatch];
+    int dst[kBatch];
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      const int idx = base + j * kBlock;
+      v[j] = 0.f;
+      dst[j] = -1;
+      if (idx < total) {
+        const int cl = fdiv(idx, per_c, inv_pc);
+        const int rem = idx - cl * per_c;
+        const int iy = fdiv(rem, IW, inv_iw);
+        const int ix = rem - iy * IW;
+        const int c = c0 + cl;
+        const int gy = py0 + iy;
+        const int gx = px0 + ix;
+        dst[j] = cl * ICS + rem;
+        if (c < c_end && gy < Wy && gx < Wx) v[j] = I[((size_t)c * Wy + gy) * Wx + gx];
+      }
+    }
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j)
+      if (dst[j] >= 0) Is[dst[j]] = v[j];
   }
 }
 
@@ -168,36 +183,92 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
       for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.f;
 
   for (int c0 = c_begin; c0 < c_end; c0 += CC) {
-    // Filter slice: MT rows of CC*K*K contiguous floats each.
-    for (int idx = threadIdx.x; idx < MT * FROW; idx += kBlock) {
-      const int mrow = idx / FROW;
-      const int e = idx - mrow * FROW;
-      const int m = m0 + mrow;
-      const int c = c0 + e / KK;
-      float v = 0.f;
-      if (m < a.M && c < c_end) v = F[((size_t)m * a.C + c0) * KK + e];
-      Fs[mrow * FP + e] = v;
+    // Filter slice: MT rows of CC*K*K contiguous floats each, loaded in
+    // batches of kFBatch per thread issued before their LDS writes.
+    {
+      constexpr int NF = MT * FROW;
+      constexpr int NLF = (NF + kBlock - 1) / kBlock;
+      constexpr int kFBatch = 12;
+#pragma unroll
+      for (int b = 0; b < NLF; b += kFBatch) {
+        float v[kFBatch];
+#pragma unroll
+        for (int j = 0; j < kFBatch; ++j) {
+          const int idx = threadIdx.x + (b + j) * kBlock;
+          const int mrow = idx / FROW;
+          const int e = idx - mrow * FROW;
+          const int m = m0 + mrow;
+          const int c = c0 + e / KK;
+          v[j] = 0.f;
+          if (b + j < NLF && idx < NF && m < a.M && c < c_end)
+            v[j] = F[((size_t)m * a.C + c0) * KK + e];
+        }
+#pragma unroll
+        for (int j = 0; j < kFBatch; ++j) {
+          const int idx = threadIdx.x + (b + j) * kBlock;
+          const int mrow = idx / FROW;
+          if (b + j < NLF && idx < NF) Fs[mrow * FP + (idx - mrow * FROW)] = v[j];
+        }
+      }
     }
     stage_input(Is, I, CC, c0, c_end, py0, px0, a.IH, a.IW, a.ICS, a.Wx, a.Wy);
     __syncthreads();
 
+    // The stage's k-steps (channel pair cp, filter row r, filter column s)
+    // run in chunks of L; operands of the next chunk are read from LDS while
+    // the current chunk's MFMAs issue.  The empty asm on the accumulators and
+    // the scheduling barrier keep the compiler from hoisting every LDS read
+    // of the stage (which would exhaust the registers).
+    {
+      constexpr int NQ = (CCW / 2) * KK;
+      constexpr int L = 4;
+      constexpr int NCH = (NQ + L - 1) / L;
+      float ca[L][MB], cb[L][NB], na[L][MB], nbv[L][NB];
+      auto load_chunk = [&](int ch, float (&av)[L][MB], float (&bv)[L][NB]) {
+        // The input offsets (runtime tile pitch) are re-derived per chunk;
+        // pinning the base stops the compiler from precomputing every
+        // offset of the stage into its own VGPR.
 #pragma unroll
-    for (int cp = 0; cp < CCW / 2; ++cp) {
+        for (int nb = 0; nb < NB; ++nb) asm volatile("" : "+v"(b_base[nb]));
 #pragma unroll
-      for (int r = 0; r < K; ++r) {
+        for (int l = 0; l < L; ++l) {
+          const int q = ch * L + l;
+          if (q < NQ) {
+            const int cp = q / KK, r = (q % KK) / K, s = q % K;
 #pragma unroll
-        for (int s = 0; s < K; ++s) {
-          const int boff = 2 * cp * a.ICS + r * a.IW + s;
-          float av[MB], bv[NB];
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb) av[mb] = Fs[a_base[mb] + 2 * cp * KK + r * K + s];
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) bv[nb] = Is[b_base[nb] + boff];
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb)
+            for (int mb = 0; mb < MB; ++mb) av[l][mb] = Fs[a_base[mb] + 2 * cp * KK + r * K + s];
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
-              acc[mb][nb] = __builtin_amdgcn_mfma_f32_32x32x2f32(av[mb], bv[nb], acc[mb][nb], 0, 0, 0);
+              bv[l][nb] = Is[b_base[nb] + 2 * cp * a.ICS + r * a.IW + s];
+          }
+        }
+      };
+      load_chunk(0, ca, cb);
+#pragma unroll
+      for (int ch = 0; ch < NCH; ++ch) {
+        if (ch + 1 < NCH) load_chunk(ch + 1, na, nbv);
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+          if (ch * L + l < NQ) {
+#pragma unroll
+            for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+              for (int nb = 0; nb < NB; ++nb)
+                acc[mb][nb] =
+                    __builtin_amdgcn_mfma_f32_32x32x2f32(ca[l][mb], cb[l][nb], acc[mb][nb], 0, 0, 0);
+          }
+        }
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) asm volatile("" : "+a"(acc[mb][nb]));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int l = 0; l < L; ++l) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb) ca[l][mb] = na[l][mb];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) cb[l][nb] = nbv[l][nb];
         }
       }
     }

@@ -64,7 +64,7 @@ __device__ __forceinline__ void load_row(const float4 *p, float *v) {
 template <int K, int R>
 __global__ __launch_bounds__(kBlock, 2) void single_tiled(
     const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
-    int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int vec4) {
+    int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int vec4, int ostore) {
   using S = TileShape<K, R>;
   constexpr int IH = S::IH, IW4 = S::IW4, NQ = S::NQ;
   constexpr int G = Group<K>::value;
@@ -78,29 +78,51 @@ __global__ __launch_bounds__(kBlock, 2) void single_tiled(
   const int x0 = (t % tiles_x) * kTileW;
 
   // Stage input rows [y0, y0+IH) x columns [x0, x0+4*IW4); zero outside the map.
-  // vec4: rows are 16-byte aligned (Wx % 4 == 0 and I 16-byte aligned).
+  // All of a thread's loads are issued before the first LDS write so that
+  // they are in flight together.  vec4: rows are 16-byte aligned (Wx % 4 == 0
+  // and I 16-byte aligned).
   if (vec4) {
-    for (int idx = threadIdx.x; idx < IH * IW4; idx += kBlock) {
+    constexpr int N = IH * IW4;
+    constexpr int NL = (N + kBlock - 1) / kBlock;
+    float4 v[NL];
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      const int idx = threadIdx.x + j * kBlock;
       const int iy = idx / IW4;
-      const int iq = idx - iy * IW4;
       const int gy = y0 + iy;
-      const int gx = x0 + 4 * iq;
-      float4 v = make_float4(0.f, 0.f, 0.f, 0.f);
-      if (gy < Wy && gx < Wx)
-        v = *reinterpret_cast<const float4 *>(I + (size_t)gy * Wx + gx);
-      tile[idx] = v;
+      const int gx = x0 + 4 * (idx - iy * IW4);
+      v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+      if ((NL * kBlock == N || idx < N) && gy < Wy && gx < Wx)
+        v[j] = *reinterpret_cast<const float4 *>(I + (size_t)gy * Wx + gx);
+    }
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      const int idx = threadIdx.x + j * kBlock;
+      if (NL * kBlock == N || idx < N) tile[idx] = v[j];
     }
   } else {
     float *tf = reinterpret_cast<float *>(tile);
     constexpr int IWf = IW4 * 4;
-    for (int idx = threadIdx.x; idx < IH * IWf; idx += kBlock) {
-      const int iy = idx / IWf;
-      const int ix = idx - iy * IWf;
-      const int gy = y0 + iy;
-      const int gx = x0 + ix;
-      float v = 0.f;
-      if (gy < Wy && gx < Wx) v = I[(size_t)gy * Wx + gx];
-      tf[idx] = v;
+    constexpr int N = IH * IWf;
+    constexpr int NL = (N + kBlock - 1) / kBlock;
+    constexpr int kBatch = 16;
+#pragma unroll
+    for (int b = 0; b < NL; b += kBatch) {
+      float v[kBatch];
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int idx = threadIdx.x + (b + j) * kBlock;
+        const int iy = idx / IWf;
+        const int gy = y0 + iy;
+        const int gx = x0 + (idx - iy * IWf);
+        v[j] = 0.f;
+        if (b + j < NL && idx < N && gy < Wy && gx < Wx) v[j] = I[(size_t)gy * Wx + gx];
+      }
+#pragma unroll
+      for (int j = 0; j < kBatch; ++j) {
+        const int idx = threadIdx.x + (b + j) * kBlock;
+        if (b + j < NL && idx < N) tf[idx] = v[j];
+      }
     }
   }
   __syncthreads();
@@ -168,11 +190,17 @@ __global__ __launch_bounds__(kBlock, 2) void single_tiled(
 #pragma unroll
       for (int j = 0; j < G; ++j) {
         const int y = oy0 + g * G + j;
-        if (y < Hout) {
-          float *orow = Om + (size_t)y * Wout;
+        if (y >= Hout) continue;
+        float *orow = Om + (size_t)y * Wout + ox0;
+        if (ox0 + kW <= Wout && ostore == 4) {
+          *reinterpret_cast<float4 *>(orow) = make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
+        } else if (ox0 + kW <= Wout && ostore == 2) {
+          reinterpret_cast<float2 *>(orow)[0] = make_float2(acc[j][0], acc[j][1]);
+          reinterpret_cast<float2 *>(orow)[1] = make_float2(acc[j][2], acc[j][3]);
+        } else {
 #pragma unroll
           for (int w = 0; w < kW; ++w)
-            if (ox0 + w < Wout) orow[ox0 + w] = acc[j][w];
+            if (ox0 + w < Wout) orow[w] = acc[j][w];
         }
       }
     }
@@ -227,13 +255,25 @@ void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
   p->lds_bytes = S::LDS;
 }
 
+// Widest output store every row of O allows: 4 floats if rows start on 16-byte
+// boundaries, 2 if on 8-byte boundaries, else 1.  Lanes own 4 columns at
+// multiples of 4, so aligned rows keep every lane's store aligned.
+int store_width(const float *O, int Wout, int Hout) {
+  const uintptr_t a = reinterpret_cast<uintptr_t>(O);
+  (void)Hout;
+  if (Wout % 4 == 0 && (a & 15) == 0) return 4;
+  if (Wout % 2 == 0 && (a & 7) == 0) return 2;
+  return 1;
+}
+
 template <int K>
 hipError_t launch_tiled(const SinglePlan &p, const float *I, const float *F, float *O,
                         int Wx, int Wy, int M, hipStream_t s) {
   constexpr int R = Rows<K>::value;
   hipLaunchKernelGGL((single_tiled<K, R>), dim3(p.grid, p.grid_z), dim3(kBlock), 0, s,
                      I, F, O, Wx, Wy, M, p.tiles_x, p.grid, p.m_per_block,
-                     (int)((Wx % 4 == 0) && ((reinterpret_cast<uintptr_t>(I) & 15) == 0)));
+                     (int)((Wx % 4 == 0) && ((reinterpret_cast<uintptr_t>(I) & 15) == 0)),
+                     store_width(O, Wx - K + 1, Wy - K + 1));
   return hipGetLastError();
 }
 
