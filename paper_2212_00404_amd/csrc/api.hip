@@ -100,7 +100,7 @@ DCONV_EXPORT int dconv_single(const float *I, const float *F, float *O, int Wx, 
   int num_cu = 0;
   if ((rc = current_num_cu(&num_cu)) != DCONV_OK) return rc;
   dconv::SinglePlan p;
-  dconv::plan_single(Wx, Wy, K, M, num_cu, &p);
+  dconv::plan_single(Wx, Wy, K, M, num_cu, (reinterpret_cast<uintptr_t>(I) & 15) == 0, &p);
   const hipError_t e = dconv::launch_single(p, I, F, O, Wx, Wy, M, (hipStream_t)stream);
   return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
 }
@@ -158,7 +158,7 @@ DCONV_EXPORT int dconv_plan_single(int Wx, int Wy, int K, int M, int num_cu, dco
   const int rc = validate_sizes(1, M, Wx, Wy, K);
   if (rc != DCONV_OK) return rc;
   dconv::SinglePlan p;
-  dconv::plan_single(Wx, Wy, K, M, num_cu > 0 ? num_cu : 256, &p);
+  dconv::plan_single(Wx, Wy, K, M, num_cu > 0 ? num_cu : 256, true, &p);
   export_single(p, out);
   return DCONV_OK;
 }

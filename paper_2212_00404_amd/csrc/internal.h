@@ -25,7 +25,7 @@ __device__ __forceinline__ int xcd_remap(int b, int n) {
 // Single-map kernels (Eq. 2)
 // ---------------------------------------------------------------------------
 struct SinglePlan {
-  int kernel;     // 0: tiled LDS kernel for K <= kMaxTiledK, 1: generic
+  int kernel;     // 0: tiled (float4 rows), 1: generic, 2: tiled (unaligned rows)
   int K;
   int rows;       // output rows per lane (R)
   int tile_h, tile_w;
@@ -39,7 +39,9 @@ struct SinglePlan {
 
 constexpr int kMaxTiledK = 11;
 
-void plan_single(int Wx, int Wy, int K, int M, int num_cu, SinglePlan *p);
+// aligned: the input map pointer is 16-byte aligned (with Wx % 4 == 0 the
+// tiled kernel then stages whole float4).
+void plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, SinglePlan *p);
 hipError_t launch_single(const SinglePlan &p, const float *I, const float *F, float *O,
                          int Wx, int Wy, int M, hipStream_t s);
 

@@ -3,21 +3,26 @@
 // One input map I[Wy][Wx], M filters F[M][K][K], output O[M][Hout][Wout].
 //
 // Design for gfx950 (the paper's SM partitioning for Pascal is prior art):
-//  * A 256-thread workgroup owns a TH x 256 output tile (TH = 4 waves x R
-//    rows).  It stages the input tile plus its K-1 halo rows and columns
-//    (Section 3.1 adds the same K-1 extra lines to each map piece) in LDS
-//    with coalesced float4 loads, then applies its share of the M filters to
-//    the staged tile one after another, so the map is fetched from HBM once
-//    per filter group (the map-split method of Section 3.1).
+//  * The output is cut into TH x 256 tiles (TH = 4 waves x R rows).  A tile
+//    needs its input rows plus K-1 halo rows and columns (Section 3.1 adds the
+//    same K-1 extra lines to each map piece).
+//  * Workgroups are persistent: each walks every nwg-th tile and, while it
+//    computes one tile from LDS, the global loads of its next tile are
+//    already in flight into registers (the prefetching of Section 2.2,
+//    method 1, done per workgroup).  After the compute the prefetched tile is
+//    written to LDS.  Blocks are remapped per XCD so that neighbouring tiles,
+//    which share halo rows, run on the same L2.
 //  * Each lane owns 4 adjacent output columns x R output rows and streams the
-//    R+K-1 input rows of its strip through registers: every row it reads from
-//    LDS (W+K-1 values, 16-byte reads) feeds up to K filter rows x K taps x 4
-//    columns of FMAs, so LDS traffic stays far below the FMA rate.
-//  * The filter is wave-uniform; the compiler keeps it in scalar registers
-//    (or VGPRs when K*K exceeds the scalar budget) and every FMA takes it as
-//    an operand directly.
-//  * Blocks are remapped so that each XCD walks a contiguous band of tiles
-//    and halo rows shared by vertically adjacent tiles stay in one L2.
+//    input rows of its strip through registers G output rows at a time: one
+//    16-byte LDS read per 4 input columns feeds up to K filter rows x K taps x
+//    4 columns of FMAs, so LDS traffic stays far below the FMA rate.
+//  * The filter is wave-uniform: up to 7x7 it stays in scalar registers and
+//    every FMA takes it as an operand; larger filters are held in VGPRs.
+//  * The filters of a workgroup (its share of the M filters) are applied to
+//    each staged tile in turn, so the map is read from HBM once per filter
+//    group (the map-split method of Section 3.1).
+#include <type_traits>
+
 #include "internal.h"
 
 namespace dconv {
@@ -29,11 +34,18 @@ constexpr int kWaves = 4;
 constexpr int kBlock = kLanes * kWaves;
 constexpr int kTileW = kLanes * kW;  // 256 output columns per tile
 
-// Output rows per lane, per filter size: enough rows that halo re-reads stay
-// small, few enough that accumulators + filter + one input row fit in VGPRs.
-template <int K> struct Rows { static constexpr int value = 8; };
+typedef float vf4 __attribute__((ext_vector_type(4)));
+typedef float vf2 __attribute__((ext_vector_type(2)));
+
+// Output rows per lane: enough that halo re-reads stay small, few enough that
+// accumulators, filter, input rows and the prefetched tile fit in VGPRs (a
+// tile prefetched as single floats takes four times the registers of one
+// prefetched as float4, so unaligned maps get shorter tiles for large K).
+template <int K, bool VEC4> struct Rows { static constexpr int value = (!VEC4 && K >= 8) ? 4 : 8; };
 // Output rows accumulated at once (a divisor of Rows).
 template <int K> struct Group { static constexpr int value = 4; };
+// Workgroups per compute unit the kernel is compiled for (register budget).
+template <int K> struct Occupancy { static constexpr int value = K <= 7 ? 4 : 2; };
 
 // Up to 7x7 the filter fits the scalar register file next to the addressing
 // state.  Larger filters would spill scalar registers into VGPR lanes inside
@@ -49,6 +61,55 @@ struct TileShape {
   static constexpr int LDS = IH * IW4 * 16;
 };
 
+// Barrier for LDS hand-over inside a workgroup.  Unlike __syncthreads() it
+// does not wait for outstanding global loads (the next tile's prefetch stays
+// in flight across it) or global stores.
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Loads of one staged tile held in registers between fetch() and commit().
+// VEC4: every map row starts on a 16-byte boundary, so whole float4 are
+// loaded; otherwise single floats.  Values outside the map are zero.
+template <int K, int R, bool VEC4>
+struct Stager {
+  using S = TileShape<K, R>;
+  using T = typename std::conditional<VEC4, float4, float>::type;
+  static constexpr int PER_ROW = VEC4 ? S::IW4 : S::IW4 * 4;
+  static constexpr int N = S::IH * PER_ROW;
+  static constexpr int NL = (N + kBlock - 1) / kBlock;
+  T v[NL];
+
+  __device__ __forceinline__ void fetch(const float *__restrict__ I, int Wx, int Wy, int y0, int x0) {
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      const int idx = threadIdx.x + j * kBlock;
+      const int iy = idx / PER_ROW;
+      const int ix = idx - iy * PER_ROW;
+      const int gy = y0 + iy;
+      const bool ok = (NL * kBlock == N || idx < N) && gy < Wy;
+      if constexpr (VEC4) {
+        const int gx = x0 + 4 * ix;
+        v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
+        if (ok && gx < Wx) v[j] = *reinterpret_cast<const float4 *>(I + (size_t)gy * Wx + gx);
+      } else {
+        const int gx = x0 + ix;
+        v[j] = 0.f;
+        if (ok && gx < Wx) v[j] = I[(size_t)gy * Wx + gx];
+      }
+    }
+  }
+
+  __device__ __forceinline__ void commit(float4 *tile) const {
+    T *dst = reinterpret_cast<T *>(tile);
+#pragma unroll
+    for (int j = 0; j < NL; ++j) {
+      const int idx = threadIdx.x + j * kBlock;
+      if (NL * kBlock == N || idx < N) dst[idx] = v[j];
+    }
+  }
+};
+
 template <int NQ>
 __device__ __forceinline__ void load_row(const float4 *p, float *v) {
 #pragma unroll
@@ -61,149 +122,134 @@ __device__ __forceinline__ void load_row(const float4 *p, float *v) {
   }
 }
 
+template <int K>
+__device__ __forceinline__ void load_filter(const float *__restrict__ F, int m, float (&f)[K][K]) {
+  const float *Fm = F + (size_t)m * K * K;
+#pragma unroll
+  for (int r = 0; r < K; ++r)
+#pragma unroll
+    for (int s = 0; s < K; ++s) {
+      f[r][s] = Fm[r * K + s];
+      if constexpr (FilterInVgpr<K>::value) asm volatile("" : "+v"(f[r][s]));
+    }
+}
+
+// One filter over the staged tile: this lane's R x 4 outputs at (oy0, ox0).
 template <int K, int R>
-__global__ __launch_bounds__(kBlock, 2) void single_tiled(
-    const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
-    int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int vec4, int ostore) {
+__device__ __forceinline__ void apply_filter(const float4 *rowp, const float (&f)[K][K],
+                                             float *__restrict__ Om, int oy0, int ox0, int Hout,
+                                             int Wout, int ostore) {
   using S = TileShape<K, R>;
-  constexpr int IH = S::IH, IW4 = S::IW4, NQ = S::NQ;
+  constexpr int IW4 = S::IW4, NQ = S::NQ;
   constexpr int G = Group<K>::value;
   static_assert(R % G == 0, "group must divide the strip");
-  __shared__ float4 tile[IH * IW4];
-
-  const int Hout = Wy - K + 1;
-  const int Wout = Wx - K + 1;
-  const int t = xcd_remap(blockIdx.x, ntiles);
-  const int y0 = (t / tiles_x) * S::TH;
-  const int x0 = (t % tiles_x) * kTileW;
-
-  // Stage input rows [y0, y0+IH) x columns [x0, x0+4*IW4); zero outside the map.
-  // All of a thread's loads are issued before the first LDS write so that
-  // they are in flight together.  vec4: rows are 16-byte aligned (Wx % 4 == 0
-  // and I 16-byte aligned).
-  if (vec4) {
-    constexpr int N = IH * IW4;
-    constexpr int NL = (N + kBlock - 1) / kBlock;
-    float4 v[NL];
-#pragma unroll
-    for (int j = 0; j < NL; ++j) {
-      const int idx = threadIdx.x + j * kBlock;
-      const int iy = idx / IW4;
-      const int gy = y0 + iy;
-      const int gx = x0 + 4 * (idx - iy * IW4);
-      v[j] = make_float4(0.f, 0.f, 0.f, 0.f);
-      if ((NL * kBlock == N || idx < N) && gy < Wy && gx < Wx)
-        v[j] = *reinterpret_cast<const float4 *>(I + (size_t)gy * Wx + gx);
-    }
-#pragma unroll
-    for (int j = 0; j < NL; ++j) {
-      const int idx = threadIdx.x + j * kBlock;
-      if (NL * kBlock == N || idx < N) tile[idx] = v[j];
-    }
-  } else {
-    float *tf = reinterpret_cast<float *>(tile);
-    constexpr int IWf = IW4 * 4;
-    constexpr int N = IH * IWf;
-    constexpr int NL = (N + kBlock - 1) / kBlock;
-    constexpr int kBatch = 16;
-#pragma unroll
-    for (int b = 0; b < NL; b += kBatch) {
-      float v[kBatch];
-#pragma unroll
-      for (int j = 0; j < kBatch; ++j) {
-        const int idx = threadIdx.x + (b + j) * kBlock;
-        const int iy = idx / IWf;
-        const int gy = y0 + iy;
-        const int gx = x0 + (idx - iy * IWf);
-        v[j] = 0.f;
-        if (b + j < NL && idx < N && gy < Wy && gx < Wx) v[j] = I[(size_t)gy * Wx + gx];
-      }
-#pragma unroll
-      for (int j = 0; j < kBatch; ++j) {
-        const int idx = threadIdx.x + (b + j) * kBlock;
-        if (b + j < NL && idx < N) tf[idx] = v[j];
-      }
-    }
-  }
-  __syncthreads();
-
-  const int lane = threadIdx.x & (kLanes - 1);
-  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
-  const float4 *rowp = tile + wave * R * IW4 + lane;
-  const int oy0 = y0 + wave * R;
-  const int ox0 = x0 + lane * kW;
-
-  const int m_begin = blockIdx.y * m_per_block;
-  const int m_end = min(M, m_begin + m_per_block);
-  for (int m = m_begin; m < m_end; ++m) {
-    const float *Fm = F + (size_t)m * K * K;
-    float f[K][K];
-#pragma unroll
-    for (int r = 0; r < K; ++r)
-#pragma unroll
-      for (int s = 0; s < K; ++s) {
-        f[r][s] = Fm[r * K + s];
-        if constexpr (FilterInVgpr<K>::value) asm volatile("" : "+v"(f[r][s]));
-      }
-
-    // Rows of the strip are processed G at a time; each group streams its
-    // G+K-1 input rows once and keeps G x 4 accumulators.
 #pragma unroll 1
-    for (int g = 0; g < R / G; ++g) {
-      const float4 *gp = rowp + g * G * IW4;
-      float acc[G][kW];
+  for (int g = 0; g < R / G; ++g) {
+    const float4 *gp = rowp + g * G * IW4;
+    float acc[G][kW];
+#pragma unroll
+    for (int j = 0; j < G; ++j)
+#pragma unroll
+      for (int w = 0; w < kW; ++w) acc[j][w] = 0.f;
+
+    // One row of look-ahead: the next input row is requested from LDS
+    // before the current one is consumed.  The accumulators pass through an
+    // empty asm statement and a scheduling barrier ends each row, which
+    // keeps the compiler from hoisting every row's reads (and exhausting the
+    // VGPRs).
+    float cur[NQ * 4], nxt[NQ * 4];
+    load_row<NQ>(gp, cur);
+#pragma unroll
+    for (int yy = 0; yy < G + K - 1; ++yy) {
+      if (yy + 1 < G + K - 1) load_row<NQ>(gp + (yy + 1) * IW4, nxt);
+#pragma unroll
+      for (int r = 0; r < K; ++r) {
+        const int j = yy - r;  // output row fed by filter row r
+        if (j < 0 || j >= G) continue;
+#pragma unroll
+        for (int s = 0; s < K; ++s)
+#pragma unroll
+          for (int w = 0; w < kW; ++w)
+            acc[j][w] = __builtin_fmaf(cur[w + s], f[r][s], acc[j][w]);
+      }
 #pragma unroll
       for (int j = 0; j < G; ++j)
 #pragma unroll
-        for (int w = 0; w < kW; ++w) acc[j][w] = 0.f;
+        for (int w = 0; w < kW; ++w) asm volatile("" : "+v"(acc[j][w]));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int q = 0; q < NQ * 4; ++q) cur[q] = nxt[q];
+    }
 
-      // One row of look-ahead: the next input row is requested from LDS
-      // before the current one is consumed; the scheduling barrier keeps the
-      // compiler from hoisting every row (which would exhaust the VGPRs).
-      float cur[NQ * 4], nxt[NQ * 4];
-      load_row<NQ>(gp, cur);
 #pragma unroll
-      for (int yy = 0; yy < G + K - 1; ++yy) {
-        if (yy + 1 < G + K - 1) load_row<NQ>(gp + (yy + 1) * IW4, nxt);
+    for (int j = 0; j < G; ++j) {
+      const int y = oy0 + g * G + j;
+      if (y >= Hout) continue;
+      // The output is written once and never read back by this kernel:
+      // non-temporal stores keep it from displacing the input tiles and
+      // halos in the caches (measured: 15-20% faster across K).
+      float *orow = Om + (size_t)y * Wout + ox0;
+      if (ox0 + kW <= Wout && ostore == 4) {
+        __builtin_nontemporal_store((vf4){acc[j][0], acc[j][1], acc[j][2], acc[j][3]},
+                                    reinterpret_cast<vf4 *>(orow));
+      } else if (ox0 + kW <= Wout && ostore == 2) {
+        __builtin_nontemporal_store((vf2){acc[j][0], acc[j][1]}, reinterpret_cast<vf2 *>(orow));
+        __builtin_nontemporal_store((vf2){acc[j][2], acc[j][3]}, reinterpret_cast<vf2 *>(orow) + 1);
+      } else {
 #pragma unroll
-        for (int r = 0; r < K; ++r) {
-          const int j = yy - r;  // output row fed by filter row r
-          if (j < 0 || j >= G) continue;
-#pragma unroll
-          for (int s = 0; s < K; ++s)
-#pragma unroll
-            for (int w = 0; w < kW; ++w)
-              acc[j][w] = __builtin_fmaf(cur[w + s], f[r][s], acc[j][w]);
-        }
-        // Pin this row's FMAs before the barrier (the accumulators pass
-        // through an empty asm statement, which is ordered like the barrier).
-#pragma unroll
-        for (int j = 0; j < G; ++j)
-#pragma unroll
-          for (int w = 0; w < kW; ++w) asm volatile("" : "+v"(acc[j][w]));
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int q = 0; q < NQ * 4; ++q) cur[q] = nxt[q];
-      }
-
-      float *Om = O + (size_t)m * Hout * Wout;
-#pragma unroll
-      for (int j = 0; j < G; ++j) {
-        const int y = oy0 + g * G + j;
-        if (y >= Hout) continue;
-        float *orow = Om + (size_t)y * Wout + ox0;
-        if (ox0 + kW <= Wout && ostore == 4) {
-          *reinterpret_cast<float4 *>(orow) = make_float4(acc[j][0], acc[j][1], acc[j][2], acc[j][3]);
-        } else if (ox0 + kW <= Wout && ostore == 2) {
-          reinterpret_cast<float2 *>(orow)[0] = make_float2(acc[j][0], acc[j][1]);
-          reinterpret_cast<float2 *>(orow)[1] = make_float2(acc[j][2], acc[j][3]);
-        } else {
-#pragma unroll
-          for (int w = 0; w < kW; ++w)
-            if (ox0 + w < Wout) orow[w] = acc[j][w];
-        }
+        for (int w = 0; w < kW; ++w)
+          if (ox0 + w < Wout) __builtin_nontemporal_store(acc[j][w], orow + w);
       }
     }
+  }
+}
+
+template <int K, int R, bool VEC4>
+__global__ __launch_bounds__(kBlock, Occupancy<K>::value) void single_tiled(
+    const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
+    int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int ostore) {
+  using S = TileShape<K, R>;
+  __shared__ float4 tile[S::IH * S::IW4];
+
+  const int Hout = Wy - K + 1;
+  const int Wout = Wx - K + 1;
+  // Persistent workgroup: tiles wg, wg + nwg, wg + 2 nwg, ...  At any moment
+  // the workgroups in flight cover one contiguous band of tiles (rows of the
+  // map), which measured faster than giving each workgroup its own run.
+  const int nwg = gridDim.x;
+  const int wg = xcd_remap(blockIdx.x, nwg);
+  if (wg >= ntiles) return;
+  const int m_begin = blockIdx.y * m_per_block;
+  const int m_end = min(M, m_begin + m_per_block);
+
+  const int lane = threadIdx.x & (kLanes - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
+  const float4 *rowp = tile + wave * R * S::IW4 + lane;
+
+  Stager<K, R, VEC4> st;
+  st.fetch(I, Wx, Wy, (wg / tiles_x) * S::TH, (wg % tiles_x) * kTileW);
+  st.commit(tile);
+  lds_barrier();
+
+  float f[K][K];
+  load_filter<K>(F, m_begin, f);
+  for (int t = wg; t < ntiles; t += nwg) {
+    const int y0 = (t / tiles_x) * S::TH;
+    const int x0 = (t % tiles_x) * kTileW;
+    const int tn = t + nwg;
+    const bool more = tn < ntiles;
+    if (more) st.fetch(I, Wx, Wy, (tn / tiles_x) * S::TH, (tn % tiles_x) * kTileW);
+
+    for (int m = m_begin; m < m_end; ++m) {
+      if (m != m_begin) load_filter<K>(F, m, f);
+      apply_filter<K, R>(rowp, f, O + (size_t)m * Hout * Wout, y0 + wave * R, x0 + lane * kW,
+                         Hout, Wout, ostore);
+    }
+    if (m_end - m_begin > 1) load_filter<K>(F, m_begin, f);
+
+    lds_barrier();  // every wave is done reading this tile
+    if (more) st.commit(tile);
+    lds_barrier();  // the next tile is in LDS
   }
 }
 
@@ -231,26 +277,30 @@ __global__ __launch_bounds__(256) void single_generic(
   O[idx] = acc;
 }
 
-template <int K>
+template <int K, bool VEC4>
 void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
-  constexpr int R = Rows<K>::value;
+  constexpr int R = Rows<K, VEC4>::value;
   using S = TileShape<K, R>;
   const int Hout = Wy - K + 1, Wout = Wx - K + 1;
-  p->kernel = 0;
+  p->kernel = VEC4 ? 0 : 2;
   p->rows = R;
   p->tile_h = S::TH;
   p->tile_w = kTileW;
   p->tiles_x = (Wout + kTileW - 1) / kTileW;
   p->tiles_y = (Hout + S::TH - 1) / S::TH;
-  p->grid = p->tiles_x * p->tiles_y;
-  // Filters reuse the staged tile; split them over workgroups only as far as
-  // needed to give every compute unit several workgroups.
-  const int want = 4 * num_cu;
-  int splits = (want + p->grid - 1) / p->grid;
+  const int ntiles = p->tiles_x * p->tiles_y;
+  // Persistent workgroups: as many as fit on the chip at once.  Filters
+  // reuse the staged tile; they are split over workgroups only as far as
+  // needed to fill the chip when there are fewer tiles than slots.
+  const int slots = Occupancy<K>::value * num_cu;
+  int splits = (slots + ntiles - 1) / ntiles;
   if (splits > M) splits = M;
   if (splits < 1) splits = 1;
   p->m_per_block = (M + splits - 1) / splits;
   p->grid_z = (M + p->m_per_block - 1) / p->m_per_block;
+  int per_split = slots / p->grid_z;
+  if (per_split < 1) per_split = 1;
+  p->grid = ntiles < per_split ? ntiles : per_split;
   p->block = kBlock;
   p->lds_bytes = S::LDS;
 }
@@ -258,9 +308,8 @@ void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
 // Widest output store every row of O allows: 4 floats if rows start on 16-byte
 // boundaries, 2 if on 8-byte boundaries, else 1.  Lanes own 4 columns at
 // multiples of 4, so aligned rows keep every lane's store aligned.
-int store_width(const float *O, int Wout, int Hout) {
+int store_width(const float *O, int Wout) {
   const uintptr_t a = reinterpret_cast<uintptr_t>(O);
-  (void)Hout;
   if (Wout % 4 == 0 && (a & 15) == 0) return 4;
   if (Wout % 2 == 0 && (a & 7) == 0) return 2;
   return 1;
@@ -269,23 +318,31 @@ int store_width(const float *O, int Wout, int Hout) {
 template <int K>
 hipError_t launch_tiled(const SinglePlan &p, const float *I, const float *F, float *O,
                         int Wx, int Wy, int M, hipStream_t s) {
-  constexpr int R = Rows<K>::value;
-  hipLaunchKernelGGL((single_tiled<K, R>), dim3(p.grid, p.grid_z), dim3(kBlock), 0, s,
-                     I, F, O, Wx, Wy, M, p.tiles_x, p.grid, p.m_per_block,
-                     (int)((Wx % 4 == 0) && ((reinterpret_cast<uintptr_t>(I) & 15) == 0)),
-                     store_width(O, Wx - K + 1, Wy - K + 1));
+  const int ostore = store_width(O, Wx - K + 1);
+  const int ntiles = p.tiles_x * p.tiles_y;
+  if (p.kernel == 0)
+    hipLaunchKernelGGL((single_tiled<K, Rows<K, true>::value, true>), dim3(p.grid, p.grid_z),
+                       dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block,
+                       ostore);
+  else
+    hipLaunchKernelGGL((single_tiled<K, Rows<K, false>::value, false>), dim3(p.grid, p.grid_z),
+                       dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block,
+                       ostore);
   return hipGetLastError();
 }
 
 }  // namespace
 
-void plan_single(int Wx, int Wy, int K, int M, int num_cu, SinglePlan *p) {
+void plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, SinglePlan *p) {
   *p = SinglePlan{};
   p->K = K;
+  // 16-byte aligned rows: whole float4 staging loads.
+  const bool vec4 = aligned && (Wx % 4 == 0);
   switch (K) {
-#define DCONV_PLAN_K(k) \
-  case k:               \
-    plan_tiled<k>(Wx, Wy, M, num_cu, p); \
+#define DCONV_PLAN_K(k)                                              \
+  case k:                                                            \
+    if (vec4) plan_tiled<k, true>(Wx, Wy, M, num_cu, p);             \
+    else plan_tiled<k, false>(Wx, Wy, M, num_cu, p);                 \
     return;
     DCONV_PLAN_K(1) DCONV_PLAN_K(2) DCONV_PLAN_K(3) DCONV_PLAN_K(4) DCONV_PLAN_K(5)
     DCONV_PLAN_K(6) DCONV_PLAN_K(7) DCONV_PLAN_K(8) DCONV_PLAN_K(9) DCONV_PLAN_K(10)
@@ -295,7 +352,7 @@ void plan_single(int Wx, int Wy, int K, int M, int num_cu, SinglePlan *p) {
       break;
   }
   const int64_t total = (int64_t)M * (Wy - K + 1) * (Wx - K + 1);
-  p->kernel = 1;
+  p->kernel = 1;  // generic
   p->rows = 1;
   p->tile_h = 1;
   p->tile_w = 256;
@@ -310,7 +367,7 @@ void plan_single(int Wx, int Wy, int K, int M, int num_cu, SinglePlan *p) {
 
 hipError_t launch_single(const SinglePlan &p, const float *I, const float *F, float *O,
                          int Wx, int Wy, int M, hipStream_t s) {
-  if (p.kernel == 1) {
+  if (p.kernel == 1) {  // generic
     hipLaunchKernelGGL(single_generic, dim3(p.grid), dim3(256), 0, s, I, F, O, Wx, Wy, p.K, M);
     return hipGetLastError();
   }

@@ -103,6 +103,25 @@ def _stream(device) -> ctypes.c_void_p:
     return ctypes.c_void_p(torch.cuda.current_stream(device).cuda_stream)
 
 
+class _OnDevice:
+    """Make ``device`` current for the C call (the library launches on the
+    current HIP device); a no-op when it already is."""
+
+    def __init__(self, device):
+        self.index = device.index if device.index is not None else torch.cuda.current_device()
+        self.prev = None
+
+    def __enter__(self):
+        cur = torch.cuda.current_device()
+        if cur != self.index:
+            self.prev = cur
+            torch.cuda.set_device(self.index)
+
+    def __exit__(self, *exc):
+        if self.prev is not None:
+            torch.cuda.set_device(self.prev)
+
+
 def single(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
     """Eq. 2: ``I[Wy, Wx]``, ``F[M, K, K]`` -> ``O[M, Wy-K+1, Wx-K+1]`` (fp32)."""
     _require(I, "I", 2)
@@ -122,7 +141,7 @@ def single(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None) ->
         _require(out, "out", 3)
         if tuple(out.shape) != shape or out.device != I.device:
             raise ValueError("out must be %r on %s" % (shape, I.device))
-    with torch.cuda.device(I.device):
+    with _OnDevice(I.device):
         rc = load().dconv_single(I.data_ptr(), F.data_ptr(), out.data_ptr(), Wx, Wy, K, M,
                                  _stream(I.device))
     _check(rc)
@@ -154,7 +173,7 @@ def multi(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None,
         _require(out, "out", 3)
         if tuple(out.shape) != shape or out.device != I.device:
             raise ValueError("out must be %r on %s" % (shape, I.device))
-    with torch.cuda.device(I.device):
+    with _OnDevice(I.device):
         rc = load().dconv_multi_variant(I.data_ptr(), F.data_ptr(), out.data_ptr(), C, M, Wx, Wy,
                                         K, _VARIANTS[variant], _stream(I.device))
     _check(rc)

@@ -98,10 +98,11 @@ def _check_single_plan(Wx, Wy, K, M):
     Hout, Wout = Wy - K + 1, Wx - K + 1
     assert p["lds_bytes"] <= LDS_MAX
     assert p["block"] in (64, 128, 256, 512, 1024)
-    if p["kernel"] == 0:
+    if p["kernel"] in (0, 2):   # persistent tiled kernel: each workgroup walks a run of tiles
         tiles_x = -(-Wout // p["tile_w"])
         tiles_y = -(-Hout // p["tile_h"])
-        assert p["grid_x"] == tiles_x * tiles_y
+        assert 1 <= p["grid_x"] <= tiles_x * tiles_y
+        assert p["grid_x"] * p["grid_y"] <= 4 * 256
         assert p["grid_y"] * p["tile_m"] >= M
         assert (p["grid_y"] - 1) * p["tile_m"] < M
     else:
@@ -137,7 +138,7 @@ def test_plans_for_workloads(name):
         p = _check_single_plan(w.Wx, w.Wy, w.K, w.M)
         # enough workgroups to occupy 256 compute units at the large size
         if w.Wx >= 1024:
-            assert p["grid_x"] * p["grid_y"] >= 256
+            assert p["grid_x"] * p["grid_y"] >= 2 * 256
     else:
         for v in ("auto", "valu", "mfma"):
             _check_multi_plan(w.C, w.M, w.Wx, w.Wy, w.K, v)
