@@ -40,6 +40,10 @@ def parse():
                     help="kernel family for multi-channel workloads")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-reps", type=int, default=2)
+    ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
+                                                      "COPY_WRITE_CSV"),
+                    help="write profiles/traffic.json from rocprofv3 counter CSVs of the default "
+                         "workload and of --copy-probe 512, then exit")
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="instead of convolving, copy a MIB-sized device buffer --steps "
                          "times (reference kernel for scaling HBM byte counters)")
@@ -61,6 +65,48 @@ def copy_probe(mib, steps):
     dt = (time.perf_counter() - t0) / steps
     print(json.dumps({"copy_probe_bytes_read": n * 4, "copy_probe_bytes_written": n * 4,
                       "steps": steps, "gbs": round(2 * n * 4 / dt / 1e9, 1)}), flush=True)
+
+
+def _counter_means(path):
+    """Mean Counter_Value per kernel name of a rocprofv3 counter_collection.csv."""
+    import csv
+    from collections import defaultdict
+    d = defaultdict(list)
+    for row in csv.DictReader(open(path)):
+        d[row["Kernel_Name"]].append(float(row["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in d.items()}
+
+
+def ingest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_mib):
+    """HBM bytes per launch of the single-map sweep kernels from rocprofv3
+    FETCH_SIZE / WRITE_SIZE runs (KiB per dispatch), each scaled by what the
+    same counter reads for a plain device copy of copy_mib MiB.  Returns a
+    dict keyed by workload name, tagged with the kernel source digest."""
+    import re
+    from paper_2212_00404_amd.build import source_digest
+    copy_bytes = copy_mib * (1 << 20)
+    cf, cw = _counter_means(copy_fetch_csv), _counter_means(copy_write_csv)
+    copy_kernel = max(cf, key=lambda k: cf[k])
+    fetch_scale = copy_bytes / (cf[copy_kernel] * 1024.0)
+    write_scale = copy_bytes / (cw[copy_kernel] * 1024.0)
+    f, w = _counter_means(fetch_csv), _counter_means(write_csv)
+    out = {"_calibration": {"copy_kernel": copy_kernel, "copy_bytes": copy_bytes,
+                            "fetch_kib_per_copy": cf[copy_kernel], "write_kib_per_copy": cw[copy_kernel],
+                            "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4)}}
+    digest = source_digest()
+    for kname, fk in f.items():
+        m = re.search(r"single_tiled<(\d+),", kname)
+        if not m:
+            continue
+        name = "single_4096x4096_m1_k%s" % m.group(1)
+        fb = fk * 1024.0 * fetch_scale
+        wb = w.get(kname, 0.0) * 1024.0 * write_scale
+        out[name] = {"kernel": re.search(r"single_tiled<[^>]*>", kname).group(0),
+                     "fetch_kib": round(fk, 1),
+                     "write_kib": round(w.get(kname, 0.0), 1), "fetch_bytes": round(fb),
+                     "write_bytes": round(wb), "bytes_per_launch": round(fb + wb),
+                     "source_digest": digest}
+    return out
 
 
 def traffic_for(kernel_tag):
@@ -113,6 +159,13 @@ def main():
     if args.copy_probe:
         copy_probe(args.copy_probe, args.steps)
         return
+    if args.ingest_pmc:
+        data = ingest_pmc(*args.ingest_pmc, copy_mib=512)
+        path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "traffic.json")
+        with open(path, "w") as fh:
+            json.dump(data, fh, indent=1, sort_keys=True)
+        print(json.dumps(data, indent=1, sort_keys=True))
+        return
 
     import torch
     import paper_2212_00404_amd as dc
@@ -150,7 +203,10 @@ def main():
             launch(b)
     torch.cuda.synchronize()
 
-    # Timed region: HIP events around every launch, on the launch stream.
+    # Timed region: HIP events around every launch, on the launch stream.  A
+    # GPU-side delay queued first lets the host enqueue the timed launches
+    # ahead of the GPU, so short kernels are timed back to back rather than
+    # at the pace of the Python launch path (the delay ends before `start`).
     stream = torch.cuda.current_stream(dev)
     ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in bufs] for _ in range(args.steps)]
@@ -158,6 +214,11 @@ def main():
     t0 = time.perf_counter()
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
+    launches_total = args.steps * len(bufs)
+    try:
+        torch.cuda._sleep(int(min(0.2, 6e-5 * launches_total) * 2.0e9))
+    except (AttributeError, RuntimeError):
+        pass
     start.record(stream)
     for s in range(args.steps):
         for i, b in enumerate(bufs):
@@ -194,8 +255,7 @@ def main():
     uses_mfma = (w.kind == "multi" and
                  dc.plan_multi(w.C, w.M, w.Wx, w.Wy, w.K, args.variant)["variant"] == 2)
     compute_bound = (w.flops / w.compulsory_bytes) >= ridge_unpacked
-    tag = "%s/%s" % (w.name, args.variant if w.kind == "multi" else "single")
-    traffic = traffic_for(tag)
+    traffic = traffic_for(w.name) if w.kind == "single" else None
     if compute_bound:
         achieved = w.flops / (pk["avg_us"] * 1e-6) / 1e12
         peak = PEAK_FP32_MFMA_TFLOPS if uses_mfma else PEAK_FP32_VECTOR_TFLOPS

@@ -113,30 +113,72 @@ __device__ __forceinline__ void block_coords(const TileArgs &a, int &tile, int &
 // ---------------------------------------------------------------------------
 // MFMA implicit-GEMM kernel
 // ---------------------------------------------------------------------------
-template <int K, int MB, int NB, int WM, int WN, int WC, int CC>
+typedef __attribute__((address_space(3))) void *lds_void_ptr;
+
+// Barrier for LDS hand-over inside a workgroup (waits for this wave's LDS
+// operations, not for its outstanding global memory operations).
+__device__ __forceinline__ void lds_barrier() {
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// Wait until this wave's direct global->LDS loads have landed in LDS.
+__device__ __forceinline__ void wait_lds_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
+
+// Direct global->LDS copy of one float per lane (gfx950 global_load_lds):
+// lane l of the wave writes lds_row[l]; lds_row must be wave-uniform.
+__device__ __forceinline__ void dma_f32(const float *src, float *lds_row) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void_ptr)lds_row, 4, 0, 0);
+}
+
+// Channel stride of a staged input tile: the largest (tpy+K-1)*(tpx+K-1)
+// over output tiles of at most PT pixels is K*(PT+K-1) (a 1 x PT or PT x 1
+// tile).
+constexpr int mfma_ics(int K, int PT) { return K * (PT + K - 1); }
+constexpr int mfma_buf_floats(int K, int MT, int PT, int CC) {
+  return MT * ((CC * K * K) | 1) + CC * mfma_ics(K, PT);
+}
+// Channels per stage: the largest multiple of 2*WC (a channel pair per wave
+// group and k-step), at most 16, whose two stage buffers fit in 80 KB (two
+// workgroups per CU).
+constexpr int mfma_cc(int K, int MT, int PT, int WC) {
+  int best = 2 * WC;
+  for (int cc = 2 * WC; cc <= 16; cc += 2 * WC)
+    if (2 * mfma_buf_floats(K, MT, PT, cc) * 4 <= 80 * 1024) best = cc;
+  return best;
+}
+
+template <int K, int MB, int NB, int WM, int WN, int WC>
 struct MfmaCfg {
   static constexpr int KK = K * K;
   static constexpr int MT = 32 * MB * WM;   // filters per workgroup
   static constexpr int PT = 32 * NB * WN;   // pixel lanes per workgroup tile
+  static constexpr int CC = mfma_cc(K, MT, PT, WC);  // channels per stage
   static constexpr int CCW = CC / WC;       // channels per wave group per stage
   static constexpr int FROW = CC * KK;      // staged floats per filter
-  static constexpr int FP = FROW + ((FROW % 2 == 0) ? 1 : 0);  // odd pitch
+  static constexpr int FP = FROW | 1;       // odd pitch: conflict-free A reads
   static constexpr int F_FLOATS = MT * FP;
-  static constexpr int RED_FLOATS = (WC - 1) * WM * WN * MB * NB * 16 * 64;
+  static constexpr int ICS = mfma_ics(K, PT);
+  static constexpr int BUF = F_FLOATS + CC * ICS;   // one stage buffer
+  static constexpr int RED = (WC - 1) * WM * WN * MB * NB * 1024;
+  static constexpr int BUF0 = BUF > RED ? BUF : RED;  // buffer 0 also holds the WC sums
+  static constexpr int LDS_BYTES = (BUF0 + BUF) * 4;
   static_assert(WM * WN * WC == 4, "four waves per workgroup");
   static_assert(CCW % 2 == 0, "channels are consumed in pairs");
 };
 
-template <int K, int MB, int NB, int WM, int WN, int WC, int CC>
+// Stage pipeline: while the MFMAs consume stage s from one LDS buffer, the
+// filter slice and input tile of stage s+1 stream into the other buffer with
+// direct global->LDS loads (no registers, no LDS write instructions).
+template <int K, int MB, int NB, int WM, int WN, int WC>
 __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I,
                                                      const float *__restrict__ F,
                                                      float *__restrict__ O,
                                                      float *__restrict__ ws, TileArgs a) {
-  using Cfg = MfmaCfg<K, MB, NB, WM, WN, WC, CC>;
-  constexpr int KK = Cfg::KK, MT = Cfg::MT, CCW = Cfg::CCW, FROW = Cfg::FROW, FP = Cfg::FP;
-  extern __shared__ float lds[];
-  float *Fs = lds;
-  float *Is = lds + Cfg::F_FLOATS;
+  using Cfg = MfmaCfg<K, MB, NB, WM, WN, WC>;
+  constexpr int KK = Cfg::KK, MT = Cfg::MT, CC = Cfg::CC, CCW = Cfg::CCW, FROW = Cfg::FROW;
+  constexpr int FP = Cfg::FP, ICS = Cfg::ICS, F_FLOATS = Cfg::F_FLOATS;
+  __shared__ float buf0[Cfg::BUF0];
+  __shared__ float buf1[Cfg::BUF];
 
   int tile, mt, split;
   block_coords(a, tile, mt, split);
@@ -166,12 +208,12 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     const int p = wn * 32 * NB + nb * 32 + col;
-    int off = 0;
+    int off = 0;  // padding lanes read pixel (0, 0); their results are dropped
     if (p < npix) {
       const int ty = p / a.tpx;
       off = ty * a.IW + (p - ty * a.tpx);
     }
-    b_base[nb] = (wc * CCW + half) * a.ICS + off;
+    b_base[nb] = F_FLOATS + (wc * CCW + half) * ICS + off;
   }
 
   floatx16 acc[MB][NB];
@@ -182,102 +224,118 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.f;
 
-  for (int c0 = c_begin; c0 < c_end; c0 += CC) {
-    // Filter slice: MT rows of CC*K*K contiguous floats each, loaded in
-    // batches of kFBatch per thread issued before their LDS writes.
-    {
-      constexpr int NF = MT * FROW;
-      constexpr int NLF = (NF + kBlock - 1) / kBlock;
-      constexpr int kFBatch = 12;
+  // Start the loads of the stage at channel c0 into `buf`.  Filter rows go to
+  // buf[r*FP + e], input rows to buf[F_FLOATS + cl*ICS + iy*IW + ix].  Rows of
+  // filters past M and input pixels outside the map are not loaded: they only
+  // feed outputs that are never stored.  Channels past c_end of a partial
+  // stage are zeroed, since they meet valid outputs.
+  auto issue = [&](int c0, float *buf) {
+    const int nc = min(CC, c_end - c0);
+    const int flen = nc * KK;
+    for (int r = wave; r < MT; r += 4) {
+      if (m0 + r >= a.M) break;
+      const float *src = F + ((size_t)(m0 + r) * a.C + c0) * KK;
+      float *dst = buf + r * FP;
 #pragma unroll
-      for (int b = 0; b < NLF; b += kFBatch) {
-        float v[kFBatch];
-#pragma unroll
-        for (int j = 0; j < kFBatch; ++j) {
-          const int idx = threadIdx.x + (b + j) * kBlock;
-          const int mrow = idx / FROW;
-          const int e = idx - mrow * FROW;
-          const int m = m0 + mrow;
-          const int c = c0 + e / KK;
-          v[j] = 0.f;
-          if (b + j < NLF && idx < NF && m < a.M && c < c_end)
-            v[j] = F[((size_t)m * a.C + c0) * KK + e];
-        }
-#pragma unroll
-        for (int j = 0; j < kFBatch; ++j) {
-          const int idx = threadIdx.x + (b + j) * kBlock;
-          const int mrow = idx / FROW;
-          if (b + j < NLF && idx < NF) Fs[mrow * FP + (idx - mrow * FROW)] = v[j];
-        }
+      for (int q = 0; q < FROW; q += 64)
+        if (q + lane < flen) dma_f32(src + q + lane, dst + q);
+    }
+    const int ncols = min(a.IW, a.Wx - px0);
+    const int nrows = min(a.IH, a.Wy - py0);
+    for (int cl = wave; cl < nc; cl += 4) {
+      const float *src_c = I + ((size_t)(c0 + cl) * a.Wy + py0) * a.Wx + px0;
+      float *dst_c = buf + F_FLOATS + cl * ICS;
+      for (int iy = 0; iy < nrows; ++iy) {
+        const float *src = src_c + (size_t)iy * a.Wx;
+        float *dst = dst_c + iy * a.IW;
+        for (int q = 0; q < ncols; q += 64)
+          if (q + lane < ncols) dma_f32(src + q + lane, dst + q);
       }
     }
-    stage_input(Is, I, CC, c0, c_end, py0, px0, a.IH, a.IW, a.ICS, a.Wx, a.Wy);
-    __syncthreads();
+    if (nc < CC) {
+      const int fz = FROW - flen;
+      for (int idx = threadIdx.x; idx < MT * fz; idx += kBlock) {
+        const int r = idx / fz;
+        buf[r * FP + flen + (idx - r * fz)] = 0.f;
+      }
+      for (int idx = threadIdx.x; idx < (CC - nc) * ICS; idx += kBlock)
+        buf[F_FLOATS + nc * ICS + idx] = 0.f;
+    }
+  };
 
-    // The stage's k-steps (channel pair cp, filter row r, filter column s)
-    // run in chunks of L; operands of the next chunk are read from LDS while
-    // the current chunk's MFMAs issue.  The empty asm on the accumulators and
-    // the scheduling barrier keep the compiler from hoisting every LDS read
-    // of the stage (which would exhaust the registers).
-    {
-      constexpr int NQ = (CCW / 2) * KK;
-      constexpr int L = 4;
-      constexpr int NCH = (NQ + L - 1) / L;
-      float ca[L][MB], cb[L][NB], na[L][MB], nbv[L][NB];
-      auto load_chunk = [&](int ch, float (&av)[L][MB], float (&bv)[L][NB]) {
-        // The input offsets (runtime tile pitch) are re-derived per chunk;
-        // pinning the base stops the compiler from precomputing every
-        // offset of the stage into its own VGPR.
+  // The stage's k-steps (channel pair cp, filter row r, filter column s) run
+  // in chunks of L with one chunk of operand look-ahead from LDS.  The empty
+  // asm statements on the accumulators and on the input base, and the
+  // scheduling barrier, keep the compiler from hoisting every LDS read (and
+  // every address) of the stage into registers.
+  auto compute = [&](const float *buf) {
+    constexpr int NQ = (CCW / 2) * KK;
+    constexpr int L = 4;
+    constexpr int NCH = (NQ + L - 1) / L;
+    float ca[L][MB], cb[L][NB], na[L][MB], nbv[L][NB];
+    auto load_chunk = [&](int ch, float (&av)[L][MB], float (&bv)[L][NB]) {
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) asm volatile("" : "+v"(b_base[nb]));
+      for (int nb = 0; nb < NB; ++nb) asm volatile("" : "+v"(b_base[nb]));
 #pragma unroll
-        for (int l = 0; l < L; ++l) {
-          const int q = ch * L + l;
-          if (q < NQ) {
-            const int cp = q / KK, r = (q % KK) / K, s = q % K;
+      for (int l = 0; l < L; ++l) {
+        const int q = ch * L + l;
+        if (q < NQ) {
+          const int cp = q / KK, r = (q % KK) / K, s = q % K;
 #pragma unroll
-            for (int mb = 0; mb < MB; ++mb) av[l][mb] = Fs[a_base[mb] + 2 * cp * KK + r * K + s];
+          for (int mb = 0; mb < MB; ++mb) av[l][mb] = buf[a_base[mb] + 2 * cp * KK + r * K + s];
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb)
+            bv[l][nb] = buf[b_base[nb] + 2 * cp * ICS + r * a.IW + s];
+        }
+      }
+    };
+    load_chunk(0, ca, cb);
+#pragma unroll
+    for (int ch = 0; ch < NCH; ++ch) {
+      if (ch + 1 < NCH) load_chunk(ch + 1, na, nbv);
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+        if (ch * L + l < NQ) {
+#pragma unroll
+          for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
             for (int nb = 0; nb < NB; ++nb)
-              bv[l][nb] = Is[b_base[nb] + 2 * cp * a.ICS + r * a.IW + s];
-          }
-        }
-      };
-      load_chunk(0, ca, cb);
-#pragma unroll
-      for (int ch = 0; ch < NCH; ++ch) {
-        if (ch + 1 < NCH) load_chunk(ch + 1, na, nbv);
-#pragma unroll
-        for (int l = 0; l < L; ++l) {
-          if (ch * L + l < NQ) {
-#pragma unroll
-            for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-              for (int nb = 0; nb < NB; ++nb)
-                acc[mb][nb] =
-                    __builtin_amdgcn_mfma_f32_32x32x2f32(ca[l][mb], cb[l][nb], acc[mb][nb], 0, 0, 0);
-          }
-        }
-#pragma unroll
-        for (int mb = 0; mb < MB; ++mb)
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) asm volatile("" : "+a"(acc[mb][nb]));
-        __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-        for (int l = 0; l < L; ++l) {
-#pragma unroll
-          for (int mb = 0; mb < MB; ++mb) ca[l][mb] = na[l][mb];
-#pragma unroll
-          for (int nb = 0; nb < NB; ++nb) cb[l][nb] = nbv[l][nb];
+              acc[mb][nb] =
+                  __builtin_amdgcn_mfma_f32_32x32x2f32(ca[l][mb], cb[l][nb], acc[mb][nb], 0, 0, 0);
         }
       }
+#pragma unroll
+      for (int mb = 0; mb < MB; ++mb)
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) asm volatile("" : "+a"(acc[mb][nb]));
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int l = 0; l < L; ++l) {
+#pragma unroll
+        for (int mb = 0; mb < MB; ++mb) ca[l][mb] = na[l][mb];
+#pragma unroll
+        for (int nb = 0; nb < NB; ++nb) cb[l][nb] = nbv[l][nb];
+      }
     }
-    __syncthreads();
+  };
+
+  issue(c_begin, buf0);
+  for (int c0 = c_begin; c0 < c_end; c0 += 2 * CC) {
+    wait_lds_dma();
+    lds_barrier();  // stage c0 is in buf0; buf1 is free
+    if (c0 + CC < c_end) issue(c0 + CC, buf1);
+    compute(buf0);
+    if (c0 + CC >= c_end) break;
+    wait_lds_dma();
+    lds_barrier();  // stage c0+CC is in buf1; buf0 is free
+    if (c0 + 2 * CC < c_end) issue(c0 + 2 * CC, buf0);
+    compute(buf1);
   }
 
   // Fixed-order sum of the WC channel groups through LDS.
   if constexpr (WC > 1) {
-    float *red = lds;
+    float *red = buf0;
+    lds_barrier();  // every wave is done with the stage buffers
     if (wc > 0) {
 #pragma unroll
       for (int mb = 0; mb < MB; ++mb)
@@ -288,7 +346,7 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
             red[((((wc - 1) * WM * WN + wmn) * MB + mb) * NB + nb) * 1024 + v * 64 + lane] =
                 acc[mb][nb][v];
     }
-    __syncthreads();
+    lds_barrier();
     if (wc != 0) return;
 #pragma unroll
     for (int g = 1; g < WC; ++g)
@@ -457,13 +515,22 @@ __global__ __launch_bounds__(256) void multi_generic(const float *__restrict__ I
   O[idx] = acc;
 }
 
-// O[i] = sum_{s < S} ws[s][i], added in the order s = 0, 1, ..., S-1.
+// O[i] = sum_{s < S} ws[s][i], added in the order s = 0, 1, ..., S-1.  The
+// partials are loaded eight at a time so their latencies overlap.
 __global__ __launch_bounds__(256) void split_sum(const float *__restrict__ ws,
                                                  float *__restrict__ O, int64_t n, int S) {
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
   if (i >= n) return;
-  float acc = ws[i];
-  for (int s = 1; s < S; ++s) acc += ws[(int64_t)s * n + i];
+  float acc = 0.f;
+  int s = 0;
+  for (; s + 8 <= S; s += 8) {
+    float v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) v[j] = ws[(int64_t)(s + j) * n + i];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc = (s + j == 0) ? v[j] : acc + v[j];
+  }
+  for (; s < S; ++s) acc = (s == 0) ? ws[i] : acc + ws[(int64_t)s * n + i];
   O[i] = acc;
 }
 
@@ -483,12 +550,13 @@ hipError_t allow_full_lds(Kern kern) {
 // Kernel table
 // ---------------------------------------------------------------------------
 // Each family has a few workgroup shapes; the planner picks one per call.
-struct MfmaShape { int MB, NB, WM, WN, WC, CC; };
+struct MfmaShape { int MB, NB, WM, WN, WC; };
 constexpr MfmaShape kMfmaShapes[] = {
-    {1, 2, 1, 1, 4, 16},  // 32 filters x 64 pixels, channel sum split over 4 waves
-    {1, 1, 2, 2, 1, 8},   // 64 x 64
-    {1, 2, 2, 2, 1, 8},   // 64 x 128
-    {2, 2, 2, 2, 1, 8},   // 128 x 128
+    {1, 2, 1, 1, 4},  // 32 filters x 64 pixels, channel sum split over 4 waves
+    {1, 1, 2, 2, 1},  // 64 x 64
+    {1, 2, 2, 2, 1},  // 64 x 128
+    {2, 2, 2, 2, 1},  // 128 x 128
+    {1, 1, 2, 1, 2},  // 64 x 32, channel sum split over 2 wave pairs
 };
 constexpr int kNumMfma = sizeof(kMfmaShapes) / sizeof(kMfmaShapes[0]);
 
@@ -503,9 +571,8 @@ template <int K, int S>
 hipError_t launch_mfma_shape(const MultiPlan &p, const float *I, const float *F, float *O,
                              float *ws, const TileArgs &a, hipStream_t st) {
   constexpr MfmaShape sh = kMfmaShapes[S];
-  auto kern = multi_mfma<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC, sh.CC>;
-  if (hipError_t e = allow_full_lds(kern); e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(kBlock), p.lds_bytes, st, I, F, O, ws, a);
+  auto kern = multi_mfma<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC>;
+  hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(kBlock), 0, st, I, F, O, ws, a);
   return hipGetLastError();
 }
 
@@ -517,6 +584,7 @@ hipError_t launch_mfma_k(const MultiPlan &p, const float *I, const float *F, flo
     case 1: return launch_mfma_shape<K, 1>(p, I, F, O, ws, a, st);
     case 2: return launch_mfma_shape<K, 2>(p, I, F, O, ws, a, st);
     case 3: return launch_mfma_shape<K, 3>(p, I, F, O, ws, a, st);
+    case 4: return launch_mfma_shape<K, 4>(p, I, F, O, ws, a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -568,19 +636,19 @@ TileChoice choose_tile(int Hout, int Wout, int cap) {
 }
 
 struct Candidate {
-  int kernel, MT, PT, WC, CC, mfma_per_kstep;  // per wave per (channel pair, r, s)
-  int f_floats_fixed;  // LDS floats for the filter slice (MFMA), 0 for VALU
-  int red_floats;
+  int kernel, MT, PT, WC, CC;
+  int ops_per_kstep;  // MFMAs per wave per (channel pair, r, s); VALU: FMAs per lane per (c, r, s)
+  int lds_fixed;      // static LDS bytes (MFMA family), 0 if it depends on the tile
+  int red_floats;     // LDS floats for the in-workgroup channel-group sum
 };
 
 Candidate mfma_candidate(int i, int K) {
   const MfmaShape s = kMfmaShapes[i];
-  const int KK = K * K;
-  const int frow = s.CC * KK;
-  const int fp = frow + ((frow % 2 == 0) ? 1 : 0);
-  const int MT = 32 * s.MB * s.WM;
-  return Candidate{i, MT, 32 * s.NB * s.WN, s.WC, s.CC, s.MB * s.NB, MT * fp,
-                   (s.WC - 1) * s.WM * s.WN * s.MB * s.NB * 16 * 64};
+  const int MT = 32 * s.MB * s.WM, PT = 32 * s.NB * s.WN;
+  const int CC = mfma_cc(K, MT, PT, s.WC);
+  const int buf = mfma_buf_floats(K, MT, PT, CC);
+  const int red = (s.WC - 1) * s.WM * s.WN * s.MB * s.NB * 1024;
+  return Candidate{i, MT, PT, s.WC, CC, s.MB * s.NB, ((buf > red ? buf : red) + buf) * 4, red};
 }
 
 Candidate valu_candidate(int i) {
@@ -589,8 +657,11 @@ Candidate valu_candidate(int i) {
 }
 
 // Rough time model in GPU clock cycles, used only to rank candidates.
-//   compute: per-wave inner-product cycles of the busiest compute unit
-//   staging: one exposed load latency per stage
+//   compute: inner-product cycles of the busiest SIMD (workgroups on one CU
+//            share its four SIMDs)
+//   loads:   stage bytes at ~32 B/clock per CU (filters mostly hit in L2)
+//   latency: the first stage's load (later stages overlap the MFMA family's
+//            compute; the VALU family pays it every stage)
 //   split:   partial sums written, re-read and summed by a second launch
 double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, int Wout,
                 int num_cu, const TileChoice &t, int split, int cps) {
@@ -599,19 +670,20 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, i
   const int64_t blocks = ntiles * mtiles * split;
   const int stages = (cps + cd.CC - 1) / cd.CC;
   const int kk = K * K;
-  // cycles of one wave per stage: MFMA 32x32x2 f32 = 64 cycles (2 channels);
-  // VALU fp32 FMA on 64 lanes = 4 cycles per filter value.
-  const double per_stage = mfma ? (double)(cd.CC / cd.WC / 2) * kk * cd.mfma_per_kstep * 64.0
-                                : (double)(cd.CC / cd.WC) * kk * cd.mfma_per_kstep * 4.0;
-  const int64_t waves_per_cu = (blocks + num_cu - 1) / num_cu;  // 1 wave per SIMD per block
-  const double compute = (double)waves_per_cu * stages * per_stage;
-  const double staging = (double)stages * 2500.0;
+  const double per_stage = mfma ? (double)(cd.CC / cd.WC / 2) * kk * cd.ops_per_kstep * 64.0
+                                : (double)(cd.CC / cd.WC) * kk * cd.ops_per_kstep * 4.0;
+  const double stage_bytes = 4.0 * ((double)(mfma ? cd.MT : 0) * cd.CC * kk +
+                                    (double)cd.CC * (t.tpy + K - 1) * (t.tpx + K - 1));
+  const int64_t per_cu = (blocks + num_cu - 1) / num_cu;
+  const double compute = (double)per_cu * stages * per_stage;
+  const double loads = (double)per_cu * stages * stage_bytes / 32.0;
+  const double latency = mfma ? 3000.0 : 3000.0 * stages;
   double extra = 0.0;
   if (split > 1) {
     const double bytes = 2.0 * split * (double)M * Hout * Wout * 4.0;
-    extra = 6000.0 + bytes / 2000.0;  // ~5 TB/s at 2.4 GHz ~ 2 KB per cycle
+    extra = 5000.0 + bytes / 2000.0;  // second launch; ~5 TB/s at 2.4 GHz ~ 2 KB per clock
   }
-  return compute + staging + extra;
+  return (compute > loads ? compute : loads) + latency + extra;
 }
 
 int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, MultiPlan *best) {
@@ -623,10 +695,12 @@ int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, Mult
     const Candidate cd = mfma ? mfma_candidate(i, K) : valu_candidate(i);
     const TileChoice t = choose_tile(Hout, Wout, cd.PT);
     const int IH = t.tpy + K - 1, IW = t.tpx + K - 1;
-    int ICS = IH * IW;
-    const int64_t lds_f = (int64_t)cd.f_floats_fixed + (int64_t)cd.CC * ICS;
-    const int64_t lds_floats = lds_f > cd.red_floats ? lds_f : cd.red_floats;
-    if (lds_floats * 4 > kMaxLds) continue;
+    int64_t lds_bytes = cd.lds_fixed;
+    if (!mfma) {
+      const int64_t stage = (int64_t)cd.CC * IH * IW;
+      lds_bytes = 4 * (stage > cd.red_floats ? stage : cd.red_floats);
+    }
+    if (lds_bytes > kMaxLds) continue;
     for (int split = 1; split <= 64; split *= 2) {
       // channels per split: a multiple of the stage size
       int cps = (C + split - 1) / split;
@@ -653,7 +727,7 @@ int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, Mult
         p.grid_y = 1;
         p.grid_z = 1;
         p.block = kBlock;
-        p.lds_bytes = (int)(lds_floats * 4);
+        p.lds_bytes = (int)lds_bytes;
         p.workspace_bytes = split > 1 ? (int64_t)split * M * Hout * Wout * 4 : 0;
         *best = p;
       }
