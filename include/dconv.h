@@ -33,7 +33,7 @@
  *     device, so repeated calls give bitwise identical output.
  *   - Calls on different streams may run concurrently; the library keeps no
  *     state that two calls share except an immutable per-device property
- *     cache.
+ *     cache and the per-(device, stream) workspace of dconv_multi.
  *   - Nothing is printed and the library never aborts.
  */
 #ifndef DCONV_H
@@ -74,10 +74,12 @@ int dconv_single(const float *I, const float *F, float *O, int Wx, int Wy, int K
  *   I : device, C*Wy*Wx floats    F : device, M*C*K*K floats
  *   O : device, M*(Wy-K+1)*(Wx-K+1) floats, written
  *   note the argument order (C, M, Wx, Wy, K) differs from dconv_single
- * When the planner splits the channel sum across workgroups it takes a
- * stream-ordered workspace from the device's default memory pool
- * (hipMallocAsync / hipFreeAsync on `stream`); DCONV_ENOMEM if that fails.
- * The partial sums are then added in a fixed order, so results stay
+ * When the planner splits the channel sum across workgroups the partial
+ * sums go to a workspace the library keeps per (device, stream): it is taken
+ * from the device's default memory pool with a stream-ordered allocation the
+ * first time a stream needs it (or needs more), reused by later calls on that
+ * stream, and kept until the process ends; DCONV_ENOMEM if the allocation
+ * fails.  The partial sums are added in a fixed order, so results stay
  * deterministic.  Other returns as for dconv_single.
  */
 int dconv_multi(const float *I, const float *F, float *O, int C, int M, int Wx,

@@ -5,7 +5,9 @@
 // so NULL pointers and bad sizes are reported without a device.
 #include <climits>
 #include <cstdint>
+#include <map>
 #include <mutex>
+#include <utility>
 #include <vector>
 
 #include "internal.h"
@@ -42,6 +44,21 @@ int current_num_cu(int *num_cu) {
   *num_cu = g_num_cu[dev];
   return DCONV_OK;
 }
+
+// Workspace for partial sums of a split channel sum, one per (device,
+// stream).  Calls on one stream run in stream order and may share it; calls
+// on different streams get different buffers.  A buffer only grows: the old
+// one is released with a stream-ordered free (after the work already queued
+// on that stream) and a larger one taken from the device's default pool.
+// The lock is held until the kernels that use the buffer are enqueued, so a
+// concurrent growth on the same stream is ordered after them.  Buffers live
+// until the process ends.
+struct Workspace {
+  void *ptr = nullptr;
+  size_t bytes = 0;
+};
+std::mutex g_ws_mu;
+std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
 
 // Sizes of Eq. 1: C, M, K >= 1, 1 <= K <= min(Wx, Wy) (valid mode needs at
 // least one output), and every tensor indexable with 32-bit element offsets.
@@ -118,20 +135,34 @@ DCONV_EXPORT int dconv_multi_variant(const float *I, const float *F, float *O, i
   dconv::MultiPlan p;
   if ((rc = dconv::plan_multi(C, M, Wx, Wy, K, variant, num_cu, &p)) != DCONV_OK) return rc;
   hipStream_t st = (hipStream_t)stream;
-  float *ws = nullptr;
-  if (p.workspace_bytes > 0) {
-    if (hipMallocAsync((void **)&ws, (size_t)p.workspace_bytes, st) != hipSuccess) {
-      (void)hipGetLastError();
-      return DCONV_ENOMEM;
-    }
+  if (p.workspace_bytes == 0) {
+    const hipError_t e = dconv::launch_multi(p, I, F, O, nullptr, C, M, Wx, Wy, st);
+    return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
   }
-  const hipError_t e = dconv::launch_multi(p, I, F, O, ws, C, M, Wx, Wy, st);
-  if (ws) {
-    if (hipFreeAsync(ws, st) != hipSuccess) {
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess) {
+    (void)hipGetLastError();
+    return DCONV_EHIP;
+  }
+  std::lock_guard<std::mutex> lock(g_ws_mu);
+  Workspace &w = g_ws[std::make_pair(dev, st)];
+  if (w.bytes < (size_t)p.workspace_bytes) {
+    if (w.ptr && hipFreeAsync(w.ptr, st) != hipSuccess) {
       (void)hipGetLastError();
       return DCONV_EHIP;
     }
+    w.ptr = nullptr;
+    w.bytes = 0;
+    const size_t want = (size_t)p.workspace_bytes;
+    if (hipMallocAsync(&w.ptr, want, st) != hipSuccess) {
+      (void)hipGetLastError();
+      w.ptr = nullptr;
+      return DCONV_ENOMEM;
+    }
+    w.bytes = want;
   }
+  const hipError_t e =
+      dconv::launch_multi(p, I, F, O, static_cast<float *>(w.ptr), C, M, Wx, Wy, st);
   return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
 }
 

@@ -130,19 +130,26 @@ __device__ __forceinline__ void dma_f32(const float *src, float *lds_row) {
   __builtin_amdgcn_global_load_lds(src, (lds_void_ptr)lds_row, 4, 0, 0);
 }
 
-// Channel stride of a staged input tile: the largest (tpy+K-1)*(tpx+K-1)
-// over output tiles of at most PT pixels is K*(PT+K-1) (a 1 x PT or PT x 1
-// tile).
-constexpr int mfma_ics(int K, int PT) { return K * (PT + K - 1); }
+constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
+// Staged geometry, in floats.
+//  * Filter rows: FROW = CC*K*K values per filter, copied in 64-lane chunks;
+//    row pitch FP = FROW rounded up to odd, so the 32 lanes that read one
+//    k-column of 32 filters hit 32 different banks.
+//  * Input planes: ICS floats per channel = the largest (tpy+K-1)*(tpx+K-1)
+//    over output tiles of at most PT pixels, K*(PT+K-1) (a 1 x PT or PT x 1
+//    tile), rounded up to whole 64-lane chunks so a plane is copied with
+//    unmasked chunks.
+constexpr int mfma_fp(int K, int CC) { return (CC * K * K) | 1; }
+constexpr int mfma_ics(int K, int PT) { return 64 * ceil_div(K * (PT + K - 1), 64); }
 constexpr int mfma_buf_floats(int K, int MT, int PT, int CC) {
-  return MT * ((CC * K * K) | 1) + CC * mfma_ics(K, PT);
+  return MT * mfma_fp(K, CC) + CC * mfma_ics(K, PT);
 }
 // Channels per stage: the largest multiple of 2*WC (a channel pair per wave
-// group and k-step), at most 16, whose two stage buffers fit in 80 KB (two
+// group and k-step), at most 64, whose two stage buffers fit in 80 KB (two
 // workgroups per CU).
 constexpr int mfma_cc(int K, int MT, int PT, int WC) {
   int best = 2 * WC;
-  for (int cc = 2 * WC; cc <= 16; cc += 2 * WC)
+  for (int cc = 2 * WC; cc <= 64; cc += 2 * WC)
     if (2 * mfma_buf_floats(K, MT, PT, cc) * 4 <= 80 * 1024) best = cc;
   return best;
 }
@@ -155,20 +162,28 @@ struct MfmaCfg {
   static constexpr int CC = mfma_cc(K, MT, PT, WC);  // channels per stage
   static constexpr int CCW = CC / WC;       // channels per wave group per stage
   static constexpr int FROW = CC * KK;      // staged floats per filter
-  static constexpr int FP = FROW | 1;       // odd pitch: conflict-free A reads
+  static constexpr int FP = mfma_fp(K, CC);
+  static constexpr int NCF = ceil_div(FROW, 64);       // 64-lane chunks per filter row
+  static constexpr int FREM = FROW - 64 * (NCF - 1);   // lanes used by the last chunk
   static constexpr int F_FLOATS = MT * FP;
   static constexpr int ICS = mfma_ics(K, PT);
-  static constexpr int BUF = F_FLOATS + CC * ICS;   // one stage buffer
+  static constexpr int NCI = ICS / 64;                 // most chunks an input plane needs
+  static constexpr int BUF = F_FLOATS + CC * ICS;      // one stage buffer
   static constexpr int RED = (WC - 1) * WM * WN * MB * NB * 1024;
-  static constexpr int BUF0 = BUF > RED ? BUF : RED;  // buffer 0 also holds the WC sums
+  static constexpr int BUF0 = BUF > RED ? BUF : RED;   // buffer 0 also holds the WC sums
   static constexpr int LDS_BYTES = (BUF0 + BUF) * 4;
   static_assert(WM * WN * WC == 4, "four waves per workgroup");
   static_assert(CCW % 2 == 0, "channels are consumed in pairs");
+  static_assert(MT % 4 == 0, "filter rows are shared out over four waves");
 };
 
 // Stage pipeline: while the MFMAs consume stage s from one LDS buffer, the
 // filter slice and input tile of stage s+1 stream into the other buffer with
-// direct global->LDS loads (no registers, no LDS write instructions).
+// direct global->LDS loads (no registers, no LDS write instructions).  The
+// per-lane source offsets of a stage are fixed for the whole kernel, so a
+// full stage is issued as unmasked 64-lane copies: lanes that fall outside
+// the map or past a filter row are pointed at valid elements whose values
+// only reach outputs that are never stored (or the padding of a row).
 template <int K, int MB, int NB, int WM, int WN, int WC>
 __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I,
                                                      const float *__restrict__ F,
@@ -177,6 +192,7 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
   using Cfg = MfmaCfg<K, MB, NB, WM, WN, WC>;
   constexpr int KK = Cfg::KK, MT = Cfg::MT, CC = Cfg::CC, CCW = Cfg::CCW, FROW = Cfg::FROW;
   constexpr int FP = Cfg::FP, ICS = Cfg::ICS, F_FLOATS = Cfg::F_FLOATS;
+  constexpr int NCF = Cfg::NCF, FREM = Cfg::FREM, NCI = Cfg::NCI;
   __shared__ float buf0[Cfg::BUF0];
   __shared__ float buf1[Cfg::BUF];
 
@@ -216,6 +232,26 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
     b_base[nb] = F_FLOATS + (wc * CCW + half) * ICS + off;
   }
 
+  // Per-lane source offsets of one input plane, chunk j covers plane elements
+  // [64j, 64j+64): element e is row e / IW, column e % IW of the halo tile,
+  // clamped into the map.
+  const int plane = a.IH * a.IW;
+  const int nci = (plane + 63) >> 6;
+  int ioff[NCI];
+#pragma unroll
+  for (int j = 0; j < NCI; ++j) {
+    int e = 64 * j + lane;
+    if (e >= plane) e = 0;
+    const int iy = e / a.IW;
+    const int gy = min(py0 + iy, a.Wy - 1);
+    const int gx = min(px0 + (e - iy * a.IW), a.Wx - 1);
+    ioff[j] = gy * a.Wx + gx;
+  }
+  // Filter rows handled by this wave, and their first element (clamped to a
+  // valid filter; rows past M only feed outputs that are never stored).
+  constexpr int RPW = MT / 4;
+  const size_t plane_elems = (size_t)a.Wy * a.Wx;
+
   floatx16 acc[MB][NB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
@@ -224,35 +260,46 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.f;
 
-  // Start the loads of the stage at channel c0 into `buf`.  Filter rows go to
-  // buf[r*FP + e], input rows to buf[F_FLOATS + cl*ICS + iy*IW + ix].  Rows of
-  // filters past M and input pixels outside the map are not loaded: they only
-  // feed outputs that are never stored.  Channels past c_end of a partial
-  // stage are zeroed, since they meet valid outputs.
+  // Start the loads of the stage at channel c0 into `buf`: filter rows to
+  // buf[r*FP + e], input planes to buf[F_FLOATS + cl*ICS + e].
   auto issue = [&](int c0, float *buf) {
     const int nc = min(CC, c_end - c0);
-    const int flen = nc * KK;
-    for (int r = wave; r < MT; r += 4) {
-      if (m0 + r >= a.M) break;
-      const float *src = F + ((size_t)(m0 + r) * a.C + c0) * KK;
-      float *dst = buf + r * FP;
+    if (nc == CC) {
 #pragma unroll
-      for (int q = 0; q < FROW; q += 64)
-        if (q + lane < flen) dma_f32(src + q + lane, dst + q);
-    }
-    const int ncols = min(a.IW, a.Wx - px0);
-    const int nrows = min(a.IH, a.Wy - py0);
-    for (int cl = wave; cl < nc; cl += 4) {
-      const float *src_c = I + ((size_t)(c0 + cl) * a.Wy + py0) * a.Wx + px0;
-      float *dst_c = buf + F_FLOATS + cl * ICS;
-      for (int iy = 0; iy < nrows; ++iy) {
-        const float *src = src_c + (size_t)iy * a.Wx;
-        float *dst = dst_c + iy * a.IW;
-        for (int q = 0; q < ncols; q += 64)
-          if (q + lane < ncols) dma_f32(src + q + lane, dst + q);
+      for (int i = 0; i < RPW; ++i) {
+        const int r = wave * RPW + i;
+        const float *src = F + ((size_t)min(m0 + r, a.M - 1) * a.C + c0) * KK + lane;
+        float *dst = buf + r * FP;
+#pragma unroll
+        for (int q = 0; q < NCF; ++q) {
+          if (q < NCF - 1 || FREM == 64 || lane < FREM) dma_f32(src + 64 * q, dst + 64 * q);
+        }
       }
-    }
-    if (nc < CC) {
+      for (int cl = wave; cl < CC; cl += 4) {
+        const float *src = I + (size_t)(c0 + cl) * plane_elems;
+        float *dst = buf + F_FLOATS + cl * ICS;
+#pragma unroll
+        for (int j = 0; j < NCI; ++j)
+          if (j < nci) dma_f32(src + ioff[j], dst + 64 * j);
+      }
+    } else {
+      // Partial stage (the channel range ends inside it): copy the nc
+      // channels present and zero the rest, which meet valid outputs.
+      const int flen = nc * KK;
+      for (int i = 0; i < RPW; ++i) {
+        const int r = wave * RPW + i;
+        const float *src = F + ((size_t)min(m0 + r, a.M - 1) * a.C + c0) * KK + lane;
+        float *dst = buf + r * FP;
+        for (int q = 0; q < NCF; ++q)
+          if (64 * q + lane < flen) dma_f32(src + 64 * q, dst + 64 * q);
+      }
+      for (int cl = wave; cl < nc; cl += 4) {
+        const float *src = I + (size_t)(c0 + cl) * plane_elems;
+        float *dst = buf + F_FLOATS + cl * ICS;
+#pragma unroll
+        for (int j = 0; j < NCI; ++j)
+          if (j < nci) dma_f32(src + ioff[j], dst + 64 * j);
+      }
       const int fz = FROW - flen;
       for (int idx = threadIdx.x; idx < MT * fz; idx += kBlock) {
         const int r = idx / fz;
@@ -292,9 +339,17 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
     load_chunk(0, ca, cb);
 #pragma unroll
     for (int ch = 0; ch < NCH; ++ch) {
-      if (ch + 1 < NCH) load_chunk(ch + 1, na, nbv);
+      // The look-ahead reads are issued between the two halves of this
+      // chunk's MFMAs: late enough that waiting for them at the start of the
+      // next chunk costs nothing, early enough to be in flight for half a
+      // chunk.  Scheduling barriers keep the order.
 #pragma unroll
       for (int l = 0; l < L; ++l) {
+        if (l == L / 2) {
+          __builtin_amdgcn_sched_barrier(0);
+          if (ch + 1 < NCH) load_chunk(ch + 1, na, nbv);
+          __builtin_amdgcn_sched_barrier(0);
+        }
         if (ch * L + l < NQ) {
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
@@ -552,11 +607,12 @@ hipError_t allow_full_lds(Kern kern) {
 // Each family has a few workgroup shapes; the planner picks one per call.
 struct MfmaShape { int MB, NB, WM, WN, WC; };
 constexpr MfmaShape kMfmaShapes[] = {
-    {1, 2, 1, 1, 4},  // 32 filters x 64 pixels, channel sum split over 4 waves
+    {1, 1, 2, 1, 2},  // 64 filters x 32 pixels, channel sum split over 2 wave pairs
+    {1, 2, 1, 2, 2},  // 32 x 128, channel sum split over 2 wave pairs
     {1, 1, 2, 2, 1},  // 64 x 64
     {1, 2, 2, 2, 1},  // 64 x 128
     {2, 2, 2, 2, 1},  // 128 x 128
-    {1, 1, 2, 1, 2},  // 64 x 32, channel sum split over 2 wave pairs
+    {1, 2, 1, 1, 4},  // 32 x 64, channel sum split over 4 waves
 };
 constexpr int kNumMfma = sizeof(kMfmaShapes) / sizeof(kMfmaShapes[0]);
 
@@ -585,6 +641,7 @@ hipError_t launch_mfma_k(const MultiPlan &p, const float *I, const float *F, flo
     case 2: return launch_mfma_shape<K, 2>(p, I, F, O, ws, a, st);
     case 3: return launch_mfma_shape<K, 3>(p, I, F, O, ws, a, st);
     case 4: return launch_mfma_shape<K, 4>(p, I, F, O, ws, a, st);
+    case 5: return launch_mfma_shape<K, 5>(p, I, F, O, ws, a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -657,14 +714,15 @@ Candidate valu_candidate(int i) {
 }
 
 // Rough time model in GPU clock cycles, used only to rank candidates.
-//   compute: inner-product cycles of the busiest SIMD (workgroups on one CU
-//            share its four SIMDs)
-//   loads:   stage bytes at ~32 B/clock per CU (filters mostly hit in L2)
-//   latency: the first stage's load (later stages overlap the MFMA family's
-//            compute; the VALU family pays it every stage)
-//   split:   partial sums written, re-read and summed by a second launch
+//   work:  inner-product plus per-stage bookkeeping cycles of the busiest CU
+//          (co-resident workgroups share its four SIMDs)
+//   chain: a workgroup's stages cannot run faster than the load latency
+//          (the MFMA family overlaps the next stage's loads with the current
+//          stage; the VALU family pays the latency every stage); `occ`
+//          co-resident workgroups overlap each other's chains
+//   split: partial sums written, re-read and added by a second launch
 double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, int Wout,
-                int num_cu, const TileChoice &t, int split, int cps) {
+                int num_cu, const TileChoice &t, int split, int cps, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
   const int64_t mtiles = (M + cd.MT - 1) / cd.MT;
   const int64_t blocks = ntiles * mtiles * split;
@@ -672,18 +730,23 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, i
   const int kk = K * K;
   const double per_stage = mfma ? (double)(cd.CC / cd.WC / 2) * kk * cd.ops_per_kstep * 64.0
                                 : (double)(cd.CC / cd.WC) * kk * cd.ops_per_kstep * 4.0;
-  const double stage_bytes = 4.0 * ((double)(mfma ? cd.MT : 0) * cd.CC * kk +
-                                    (double)cd.CC * (t.tpy + K - 1) * (t.tpx + K - 1));
+  const double overhead = 600.0;
+  const double latency = 3000.0;
+  int occ = (int)(160 * 1024 / (lds_bytes > 0 ? lds_bytes : 1));
+  if (occ > 4) occ = 4;
+  if (occ < 1) occ = 1;
   const int64_t per_cu = (blocks + num_cu - 1) / num_cu;
-  const double compute = (double)per_cu * stages * per_stage;
-  const double loads = (double)per_cu * stages * stage_bytes / 32.0;
-  const double latency = mfma ? 3000.0 : 3000.0 * stages;
+  const int64_t rounds = (per_cu + occ - 1) / occ;
+  const double work = (double)per_cu * stages * (per_stage + overhead);
+  const double stage_chain = mfma ? (per_stage + overhead > latency ? per_stage + overhead : latency)
+                                  : per_stage + overhead + latency;
+  const double chain = (double)rounds * stages * stage_chain;
   double extra = 0.0;
   if (split > 1) {
     const double bytes = 2.0 * split * (double)M * Hout * Wout * 4.0;
     extra = 5000.0 + bytes / 2000.0;  // second launch; ~5 TB/s at 2.4 GHz ~ 2 KB per clock
   }
-  return (compute > loads ? compute : loads) + latency + extra;
+  return (work > chain ? work : chain) + latency + 2000.0 + extra;
 }
 
 int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, MultiPlan *best) {
@@ -707,7 +770,7 @@ int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, Mult
       cps = (cps + cd.CC - 1) / cd.CC * cd.CC;
       const int real_split = (C + cps - 1) / cps;
       if (real_split != split) break;
-      const double tm = estimate(cd, mfma, C, M, K, Hout, Wout, num_cu, t, split, cps);
+      const double tm = estimate(cd, mfma, C, M, K, Hout, Wout, num_cu, t, split, cps, lds_bytes);
       if (tm < best_t) {
         best_t = tm;
         found = true;

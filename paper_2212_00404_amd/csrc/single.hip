@@ -44,8 +44,9 @@ typedef float vf2 __attribute__((ext_vector_type(2)));
 template <int K, bool VEC4> struct Rows { static constexpr int value = (!VEC4 && K >= 8) ? 4 : 8; };
 // Output rows accumulated at once (a divisor of Rows).
 template <int K> struct Group { static constexpr int value = 4; };
-// Workgroups per compute unit the kernel is compiled for (register budget).
-template <int K> struct Occupancy { static constexpr int value = K <= 7 ? 4 : 2; };
+// Workgroups per compute unit the kernel is compiled for (register budget; a
+// tile prefetched as single floats needs four times the registers).
+template <int K, bool VEC4> struct Occupancy { static constexpr int value = (VEC4 && K <= 7) ? 4 : 2; };
 
 // Up to 7x7 the filter fits the scalar register file next to the addressing
 // state.  Larger filters would spill scalar registers into VGPR lanes inside
@@ -125,13 +126,23 @@ __device__ __forceinline__ void load_row(const float4 *p, float *v) {
 template <int K>
 __device__ __forceinline__ void load_filter(const float *__restrict__ F, int m, float (&f)[K][K]) {
   const float *Fm = F + (size_t)m * K * K;
+  if constexpr (FilterInVgpr<K>::value) {
+    // Vector loads through a pointer the compiler cannot prove uniform: all
+    // K*K loads are in flight together (scalar loads of this many values
+    // would be issued and waited for one at a time).
+    int zero;
+    asm volatile("v_mov_b32 %0, 0" : "=v"(zero));
+    const float *p = Fm + zero;
 #pragma unroll
-  for (int r = 0; r < K; ++r)
+    for (int r = 0; r < K; ++r)
 #pragma unroll
-    for (int s = 0; s < K; ++s) {
-      f[r][s] = Fm[r * K + s];
-      if constexpr (FilterInVgpr<K>::value) asm volatile("" : "+v"(f[r][s]));
-    }
+      for (int s = 0; s < K; ++s) f[r][s] = p[r * K + s];
+  } else {
+#pragma unroll
+    for (int r = 0; r < K; ++r)
+#pragma unroll
+      for (int s = 0; s < K; ++s) f[r][s] = Fm[r * K + s];
+  }
 }
 
 // One filter over the staged tile: this lane's R x 4 outputs at (oy0, ox0).
@@ -205,7 +216,7 @@ __device__ __forceinline__ void apply_filter(const float4 *rowp, const float (&f
 }
 
 template <int K, int R, bool VEC4>
-__global__ __launch_bounds__(kBlock, Occupancy<K>::value) void single_tiled(
+__global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_tiled(
     const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
     int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int ostore) {
   using S = TileShape<K, R>;
@@ -292,7 +303,7 @@ void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
   // Persistent workgroups: as many as fit on the chip at once.  Filters
   // reuse the staged tile; they are split over workgroups only as far as
   // needed to fill the chip when there are fewer tiles than slots.
-  const int slots = Occupancy<K>::value * num_cu;
+  const int slots = Occupancy<K, VEC4>::value * num_cu;
   int splits = (slots + ntiles - 1) / ntiles;
   if (splits > M) splits = M;
   if (splits < 1) splits = 1;
