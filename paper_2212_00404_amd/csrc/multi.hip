@@ -141,8 +141,11 @@ constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
 //    unmasked chunks.
 constexpr int mfma_fp(int K, int CC) { return (CC * K * K) | 1; }
 constexpr int mfma_ics(int K, int PT) { return 64 * ceil_div(K * (PT + K - 1), 64); }
+// Filter rows are copied by the four waves in blocks of MT/4 consecutive
+// rows, each block followed by a 64-float gap (see the kernel's issue()).
+constexpr int mfma_fblk(int K, int MT, int CC) { return (MT / 4) * mfma_fp(K, CC) + 64; }
 constexpr int mfma_buf_floats(int K, int MT, int PT, int CC) {
-  return MT * mfma_fp(K, CC) + CC * mfma_ics(K, PT);
+  return 4 * mfma_fblk(K, MT, CC) + CC * mfma_ics(K, PT);
 }
 // Channels per stage: the largest multiple of 2*WC (a channel pair per wave
 // group and k-step), at most 64, whose two stage buffers fit in 80 KB (two
@@ -164,8 +167,9 @@ struct MfmaCfg {
   static constexpr int FROW = CC * KK;      // staged floats per filter
   static constexpr int FP = mfma_fp(K, CC);
   static constexpr int NCF = ceil_div(FROW, 64);       // 64-lane chunks per filter row
-  static constexpr int FREM = FROW - 64 * (NCF - 1);   // lanes used by the last chunk
-  static constexpr int F_FLOATS = MT * FP;
+  static constexpr int RPW = MT / 4;                   // filter rows copied per wave
+  static constexpr int FBLK = mfma_fblk(K, MT, CC);    // LDS stride of a wave's row block
+  static constexpr int F_FLOATS = 4 * FBLK;
   static constexpr int ICS = mfma_ics(K, PT);
   static constexpr int NCI = ICS / 64;                 // most chunks an input plane needs
   static constexpr int BUF = F_FLOATS + CC * ICS;      // one stage buffer
@@ -192,7 +196,7 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
   using Cfg = MfmaCfg<K, MB, NB, WM, WN, WC>;
   constexpr int KK = Cfg::KK, MT = Cfg::MT, CC = Cfg::CC, CCW = Cfg::CCW, FROW = Cfg::FROW;
   constexpr int FP = Cfg::FP, ICS = Cfg::ICS, F_FLOATS = Cfg::F_FLOATS;
-  constexpr int NCF = Cfg::NCF, FREM = Cfg::FREM, NCI = Cfg::NCI;
+  constexpr int NCF = Cfg::NCF, NCI = Cfg::NCI, RPW = Cfg::RPW, FBLK = Cfg::FBLK;
   __shared__ float buf0[Cfg::BUF0];
   __shared__ float buf1[Cfg::BUF];
 
@@ -217,8 +221,10 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
 
   int a_base[MB];
 #pragma unroll
-  for (int mb = 0; mb < MB; ++mb)
-    a_base[mb] = (wm * 32 * MB + mb * 32 + col) * FP + (wc * CCW + half) * KK;
+  for (int mb = 0; mb < MB; ++mb) {
+    const int row = wm * 32 * MB + mb * 32 + col;
+    a_base[mb] = (row / RPW) * FBLK + (row % RPW) * FP + (wc * CCW + half) * KK;
+  }
   int b_base[NB];
   const int npix = a.tpy * a.tpx;
 #pragma unroll
@@ -231,6 +237,13 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
     }
     b_base[nb] = F_FLOATS + (wc * CCW + half) * ICS + off;
   }
+  // One input address per filter row r: every B read of a stage is then
+  // b_row[nb][r] plus a compile-time offset (channel pair and column).
+  int b_row[NB][K];
+#pragma unroll
+  for (int nb = 0; nb < NB; ++nb)
+#pragma unroll
+    for (int r = 0; r < K; ++r) b_row[nb][r] = b_base[nb] + r * a.IW;
 
   // Per-lane source offsets of one input plane, chunk j covers plane elements
   // [64j, 64j+64): element e is row e / IW, column e % IW of the halo tile,
@@ -247,10 +260,23 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
     const int gx = min(px0 + (e - iy * a.IW), a.Wx - 1);
     ioff[j] = gy * a.Wx + gx;
   }
-  // Filter rows handled by this wave, and their first element (clamped to a
-  // valid filter; rows past M only feed outputs that are never stored).
-  constexpr int RPW = MT / 4;
+  // Filter rows are copied in 64-lane chunks; chunk q of a row covers row
+  // elements [64q, 64q+64).  When the last chunk's overhang stays within the
+  // next row's slot (FSPILL), its lanes past FROW land on the row's padding
+  // float or at position e of the next row's slot and copy that row's element
+  // e (element 0 for a padding float): they write what the next row's own
+  // copy writes, so the order of the two copies does not matter.  For the
+  // last row of a wave's block they land in the gap after the block and
+  // re-read the row's first element.  Otherwise the last chunk is masked.
+  constexpr bool FSPILL = 64 * NCF <= 2 * FP;
   const size_t plane_elems = (size_t)a.Wy * a.Wx;
+  const size_t frow_stride = (size_t)a.C * KK;
+  const int e_last = 64 * (NCF - 1) + lane;
+  const bool f_spill = e_last >= FROW;
+  int e_next = e_last - FP;
+  if (e_next < 0 || e_next >= FROW) e_next = 0;
+  const int ofs_last = f_spill ? (int)frow_stride + e_next : e_last;
+  const int ofs_last_end = f_spill ? 0 : e_last;
 
   floatx16 acc[MB][NB];
 #pragma unroll
@@ -260,27 +286,57 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
 #pragma unroll
       for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.f;
 
-  // Start the loads of the stage at channel c0 into `buf`: filter rows to
-  // buf[r*FP + e], input planes to buf[F_FLOATS + cl*ICS + e].
+  // Start the loads of the stage at channel c0 into `buf`: filter row r to
+  // buf[(r / RPW)*FBLK + (r % RPW)*FP + e], input planes to
+  // buf[F_FLOATS + cl*ICS + e].
   auto issue = [&](int c0, float *buf) {
     const int nc = min(CC, c_end - c0);
     if (nc == CC) {
+      // This wave's RPW consecutive filter rows, in ascending order.  The
+      // last chunk of a row may spill past FROW into the next row's first
+      // elements; copies from one wave land in issue order, so the next
+      // row's own copy (issued later) overwrites the spill, and the last
+      // row of the block spills into the 64-float gap after it.  Rows past M
+      // (last filter tile only) are clamped to filter M-1: they only feed
+      // outputs that are never stored.
+      float *dst = buf + wave * FBLK;
+      const int r0 = m0 + wave * RPW;
+      if (r0 + RPW <= a.M) {
+        const float *src = F + ((size_t)r0 * a.C + c0) * KK;
 #pragma unroll
-      for (int i = 0; i < RPW; ++i) {
-        const int r = wave * RPW + i;
-        const float *src = F + ((size_t)min(m0 + r, a.M - 1) * a.C + c0) * KK + lane;
-        float *dst = buf + r * FP;
+        for (int i = 0; i < RPW; ++i) {
 #pragma unroll
-        for (int q = 0; q < NCF; ++q) {
-          if (q < NCF - 1 || FREM == 64 || lane < FREM) dma_f32(src + 64 * q, dst + 64 * q);
+          for (int q = 0; q < NCF - 1; ++q) dma_f32(src + 64 * q + lane, dst + 64 * q);
+          if constexpr (FSPILL)
+            dma_f32(src + (i + 1 < RPW ? ofs_last : ofs_last_end), dst + 64 * (NCF - 1));
+          else if (!f_spill)
+            dma_f32(src + e_last, dst + 64 * (NCF - 1));
+          src += frow_stride;
+          dst += FP;
+        }
+      } else {
+#pragma unroll
+        for (int i = 0; i < RPW; ++i) {
+          const int rr = min(r0 + i, a.M - 1);
+          const int rn = min(r0 + i + 1, a.M - 1);
+          const float *src = F + ((size_t)rr * a.C + c0) * KK;
+#pragma unroll
+          for (int q = 0; q < NCF - 1; ++q) dma_f32(src + 64 * q + lane, dst + 64 * q);
+          const size_t spill = (i + 1 < RPW) ? (size_t)(rn - rr) * frow_stride + e_next : 0;
+          if constexpr (FSPILL)
+            dma_f32(src + (f_spill ? spill : (size_t)e_last), dst + 64 * (NCF - 1));
+          else if (!f_spill)
+            dma_f32(src + e_last, dst + 64 * (NCF - 1));
+          dst += FP;
         }
       }
+      const float *src = I + (size_t)(c0 + wave) * plane_elems;
       for (int cl = wave; cl < CC; cl += 4) {
-        const float *src = I + (size_t)(c0 + cl) * plane_elems;
-        float *dst = buf + F_FLOATS + cl * ICS;
+        float *dsti = buf + F_FLOATS + cl * ICS;
 #pragma unroll
         for (int j = 0; j < NCI; ++j)
-          if (j < nci) dma_f32(src + ioff[j], dst + 64 * j);
+          if (j < nci) dma_f32(src + ioff[j], dsti + 64 * j);
+        src += 4 * plane_elems;
       }
     } else {
       // Partial stage (the channel range ends inside it): copy the nc
@@ -289,7 +345,7 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
       for (int i = 0; i < RPW; ++i) {
         const int r = wave * RPW + i;
         const float *src = F + ((size_t)min(m0 + r, a.M - 1) * a.C + c0) * KK + lane;
-        float *dst = buf + r * FP;
+        float *dst = buf + wave * FBLK + i * FP;
         for (int q = 0; q < NCF; ++q)
           if (64 * q + lane < flen) dma_f32(src + 64 * q, dst + 64 * q);
       }
@@ -303,7 +359,7 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
       const int fz = FROW - flen;
       for (int idx = threadIdx.x; idx < MT * fz; idx += kBlock) {
         const int r = idx / fz;
-        buf[r * FP + flen + (idx - r * fz)] = 0.f;
+        buf[(r / RPW) * FBLK + (r % RPW) * FP + flen + (idx - r * fz)] = 0.f;
       }
       for (int idx = threadIdx.x; idx < (CC - nc) * ICS; idx += kBlock)
         buf[F_FLOATS + nc * ICS + idx] = 0.f;
@@ -312,17 +368,14 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
 
   // The stage's k-steps (channel pair cp, filter row r, filter column s) run
   // in chunks of L with one chunk of operand look-ahead from LDS.  The empty
-  // asm statements on the accumulators and on the input base, and the
-  // scheduling barrier, keep the compiler from hoisting every LDS read (and
-  // every address) of the stage into registers.
+  // asm statements on the accumulators and the scheduling barriers keep the
+  // compiler from hoisting every LDS read of the stage into registers.
   auto compute = [&](const float *buf) {
     constexpr int NQ = (CCW / 2) * KK;
     constexpr int L = 4;
     constexpr int NCH = (NQ + L - 1) / L;
     float ca[L][MB], cb[L][NB], na[L][MB], nbv[L][NB];
     auto load_chunk = [&](int ch, float (&av)[L][MB], float (&bv)[L][NB]) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) asm volatile("" : "+v"(b_base[nb]));
 #pragma unroll
       for (int l = 0; l < L; ++l) {
         const int q = ch * L + l;
@@ -331,8 +384,7 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb) av[l][mb] = buf[a_base[mb] + 2 * cp * KK + r * K + s];
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb)
-            bv[l][nb] = buf[b_base[nb] + 2 * cp * ICS + r * a.IW + s];
+          for (int nb = 0; nb < NB; ++nb) bv[l][nb] = buf[b_row[nb][r] + 2 * cp * ICS + s];
         }
       }
     };
