@@ -284,7 +284,8 @@ def main():
                   "Wy": w.Wy, "K": w.K, "variant": args.variant, "launches_per_step": 1}
     out = {
         "metric": METRIC, "value": round(value_gflops, 2), "unit": "GFLOP/s", "n_gpus": 1,
-        "steps": args.steps, "warmup": args.warmup, "ms_per_step": round(ms_per_step, 5),
+        "steps": args.steps, "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic", "config": config, "roofline": roof, "cpu_baseline": cpu,
         "per_kernel": per_kernel, "wall_s_timed": round(wall, 4),

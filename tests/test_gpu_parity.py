@@ -141,3 +141,44 @@ def test_every_output_written_on_a_side_stream():
     s.synchronize()
     O64, A64 = oracle_single(Is, Fs)
     assert_within(outs.cpu().numpy(), O64, A64, "side stream single")
+
+
+def test_split_workspace_reused_across_plans():
+    """Channel-split calls with different tile counts and split factors queued
+    back to back on one stream share its workspace: the arrival counters must
+    be back at zero after every call, and growth between calls must not
+    disturb queued work."""
+    shapes = [(512, 512, 9, 9, 3), (256, 256, 30, 30, 3), (64, 96, 20, 20, 3),
+              (512, 512, 9, 9, 3), (128, 128, 60, 60, 5), (256, 256, 28, 28, 1)]
+    splits = [dc.plan_multi(*s)["split_c"] for s in shapes]
+    assert sum(sp > 1 for sp in splits) >= 3, splits
+    cases = []
+    for i, (C, M, Wx, Wy, K) in enumerate(shapes):
+        I, F = random_arrays(C, M, Wx, Wy, K, seed=9000 + i, variant="int")
+        cases.append((I, F, torch.from_numpy(I).cuda(), torch.from_numpy(F).cuda()))
+    torch.cuda.synchronize()
+    outs = [dc.multi(It, Ft) for _, _, It, Ft in cases]
+    torch.cuda.synchronize()
+    for (I, F, _, _), out, s in zip(cases, outs, shapes):
+        O64, _ = oracle_multi(I, F)
+        assert_exact(out.cpu().numpy(), O64, "reuse %r" % (s,))
+
+
+def test_split_calls_on_two_streams():
+    """Concurrent channel-split calls on two streams use separate workspaces."""
+    shapes = [(512, 512, 9, 9, 3), (512, 512, 16, 16, 3)]
+    assert all(dc.plan_multi(*s)["split_c"] > 1 for s in shapes)
+    data = [random_arrays(*s, seed=9100 + i, variant="int") for i, s in enumerate(shapes)]
+    dev = [(torch.from_numpy(I).cuda(), torch.from_numpy(F).cuda()) for I, F in data]
+    streams = [torch.cuda.Stream(), torch.cuda.Stream()]
+    torch.cuda.synchronize()
+    outs = [[], []]
+    for _ in range(3):
+        for k in range(2):
+            with torch.cuda.stream(streams[k]):
+                outs[k].append(dc.multi(*dev[k]))
+    torch.cuda.synchronize()
+    for k in range(2):
+        O64, _ = oracle_multi(*data[k])
+        for o in outs[k]:
+            assert_exact(o.cpu().numpy(), O64, "stream %d" % k)
