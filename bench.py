@@ -10,8 +10,11 @@ from HBM).  ``--workload`` selects any other named workload (multi-channel
 shapes are measured the same way, one launch per step).
 
 Prints ONE JSON line: GFLOP/s over the timed steps (2*C*M*K^2*Hout*Wout
-flops per launch), the roofline of the dominant kernel measured with HIP
-events on the launch stream, and the CPU oracle timed on the host cores.
+flops per launch; the steps run back to back with HIP events only around the
+whole timed region), the per-kernel durations and the roofline of the
+dominant kernel from a second pass of the same steps with a HIP event pair
+around every launch on the launch stream, and the CPU oracle timed on the
+host cores.
 """
 import argparse
 import json
@@ -27,6 +30,9 @@ PEAK_FP32_UNPACKED_TFLOPS = 78.6     # one fp32 FMA per lane per clock
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 SWEEP = "single_4096x4096_m1_k3-11"
+# Sources the single-map kernels are built from: recorded HBM traffic stays
+# valid while these are unchanged.
+SINGLE_SOURCES = ("single.hip", "internal.h")
 
 
 def parse():
@@ -81,7 +87,8 @@ def ingest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_mib):
     """HBM bytes per launch of the single-map sweep kernels from rocprofv3
     FETCH_SIZE / WRITE_SIZE runs (KiB per dispatch), each scaled by what the
     same counter reads for a plain device copy of copy_mib MiB.  Returns a
-    dict keyed by workload name, tagged with the kernel source digest."""
+    dict keyed by workload name, tagged with the digest of the single-map
+    kernel sources (SINGLE_SOURCES)."""
     import re
     from paper_2212_00404_amd.build import source_digest
     copy_bytes = copy_mib * (1 << 20)
@@ -93,7 +100,7 @@ def ingest_pmc(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_mib):
     out = {"_calibration": {"copy_kernel": copy_kernel, "copy_bytes": copy_bytes,
                             "fetch_kib_per_copy": cf[copy_kernel], "write_kib_per_copy": cw[copy_kernel],
                             "fetch_scale": round(fetch_scale, 4), "write_scale": round(write_scale, 4)}}
-    digest = source_digest()
+    digest = source_digest(SINGLE_SOURCES)
     for kname, fk in f.items():
         m = re.search(r"single_tiled<(\d+),", kname)
         if not m:
@@ -123,7 +130,7 @@ def traffic_for(kernel_tag):
     if not ent:
         return None
     from paper_2212_00404_amd.build import source_digest
-    if ent.get("source_digest") != source_digest():
+    if ent.get("source_digest") != source_digest(SINGLE_SOURCES):
         return None
     return ent.get("bytes_per_launch")
 
@@ -147,6 +154,75 @@ def cpu_baseline(launches, reps):
             "kind": "oracle",
             "sample": "one full step (%d launch%s, %.2f GFLOP), best of %d, fp64 C oracle"
                       % (len(launches), "es" if len(launches) > 1 else "", flops / 1e9, reps)}
+
+
+class KernelEvents:
+    """HIP event pairs around each launch of the instrumented pass.
+
+    Created through the HIP runtime that torch has loaded (same soname, so
+    the same instance) with hipEventDisableSystemFence: the events only
+    time, and the device is synchronised before they are read.  Falls back
+    to torch events (default flags) if that entry point is unavailable."""
+
+    DISABLE_SYSTEM_FENCE = 0x20000000
+
+    def __init__(self, stream, steps, per_step):
+        import ctypes
+        import torch
+        self.stream = stream
+        self.kind = "hip_no_system_fence"
+        try:
+            hip = ctypes.CDLL("libamdhip64.so.7")
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                ctypes.c_void_p]
+            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+
+            def make():
+                e = ctypes.c_void_p()
+                if hip.hipEventCreateWithFlags(ctypes.byref(e), self.DISABLE_SYSTEM_FENCE) != 0:
+                    raise OSError("hipEventCreateWithFlags failed")
+                return e
+            self.hip, self.ct = hip, ctypes
+            self.ev = [[(make(), make()) for _ in range(per_step)] for _ in range(steps)]
+            self.ends = (make(), make())
+        except (OSError, AttributeError):
+            self.hip = None
+            self.kind = "torch_default"
+            mk = lambda: torch.cuda.Event(enable_timing=True)
+            self.ev = [[(mk(), mk()) for _ in range(per_step)] for _ in range(steps)]
+            self.ends = (mk(), mk())
+        self.sp = None if self.hip is None else self.ct.c_void_p(stream.cuda_stream)
+
+    def _rec(self, e):
+        if self.hip is None:
+            e.record(self.stream)
+        elif self.hip.hipEventRecord(e, self.sp) != 0:
+            raise RuntimeError("hipEventRecord failed")
+
+    def _el(self, a, b):
+        if self.hip is None:
+            return a.elapsed_time(b)
+        f = self.ct.c_float()
+        if self.hip.hipEventElapsedTime(self.ct.byref(f), a, b) != 0:
+            raise RuntimeError("hipEventElapsedTime failed")
+        return f.value
+
+    def record(self, s, i, which):
+        self._rec(self.ev[s][i][which])
+
+    def record_start(self):
+        self._rec(self.ends[0])
+
+    def record_stop(self):
+        self._rec(self.ends[1])
+
+    def elapsed_ms(self, s, i):
+        return self._el(*self.ev[s][i])
+
+    def total_ms(self):
+        return self._el(*self.ends)
 
 
 def main():
@@ -203,40 +279,60 @@ def main():
             launch(b)
     torch.cuda.synchronize()
 
-    # Timed region: HIP events around every launch, on the launch stream.  A
-    # GPU-side delay queued first lets the host enqueue the timed launches
-    # ahead of the GPU, so short kernels are timed back to back rather than
-    # at the pace of the Python launch path (the delay ends before `start`).
+    # Timed region: the K steps back to back, HIP events only at its two
+    # ends, on the launch stream.  A GPU-side delay queued first lets the
+    # host enqueue the timed launches ahead of the GPU, so short kernels run
+    # back to back rather than at the pace of the Python launch path (the
+    # delay ends before `start`).
     stream = torch.cuda.current_stream(dev)
-    ev = [[(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in bufs] for _ in range(args.steps)]
+    launches_total = args.steps * len(bufs)
+    delay_cycles = int(min(0.2, 6e-5 * launches_total) * 2.0e9)
+
+    def gpu_delay():
+        try:
+            torch.cuda._sleep(delay_cycles)
+        except (AttributeError, RuntimeError):
+            pass
+
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     start = torch.cuda.Event(enable_timing=True)
     stop = torch.cuda.Event(enable_timing=True)
-    launches_total = args.steps * len(bufs)
-    try:
-        torch.cuda._sleep(int(min(0.2, 6e-5 * launches_total) * 2.0e9))
-    except (AttributeError, RuntimeError):
-        pass
+    gpu_delay()
     start.record(stream)
     for s in range(args.steps):
-        for i, b in enumerate(bufs):
-            ev[s][i][0].record(stream)
+        for b in bufs:
             launch(b)
-            ev[s][i][1].record(stream)
     stop.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - t0
     total_ms = start.elapsed_time(stop)
     ms_per_step = total_ms / args.steps
 
+    # Per-kernel durations: the same K steps again with a HIP event pair
+    # around every launch.  An event with the default system-scope fence
+    # adds about 3 us per launch (cache write-back), so these events are
+    # created without it (timing only); they still add about 1.5 us per
+    # launch, which is why the step time above is measured without them.
+    ev = KernelEvents(stream, args.steps, len(bufs))
+    torch.cuda.synchronize()
+    gpu_delay()
+    ev.record_start()
+    for s in range(args.steps):
+        for i, b in enumerate(bufs):
+            ev.record(s, i, 0)
+            launch(b)
+            ev.record(s, i, 1)
+    ev.record_stop()
+    torch.cuda.synchronize()
+    ms_per_step_instr = ev.total_ms() / args.steps
+
     step_flops = sum(w.flops for w, _, _, _ in bufs)
     value_gflops = step_flops / (ms_per_step * 1e-3) / 1e9
 
     per_kernel = []
     for i, (w, _, _, _) in enumerate(bufs):
-        d = np.array([ev[s][i][0].elapsed_time(ev[s][i][1]) for s in range(args.steps)])
+        d = np.array([ev.elapsed_ms(s, i) for s in range(args.steps)])
         avg_s = float(d.mean()) * 1e-3
         tf = w.flops / avg_s / 1e12
         gbs = w.compulsory_bytes / avg_s / 1e9
@@ -286,6 +382,8 @@ def main():
         "metric": METRIC, "value": round(value_gflops, 2), "unit": "GFLOP/s", "n_gpus": 1,
         "steps": args.steps, "warmup": args.warmup,
         "ms_per_step": round(ms_per_step, 5),
+        "ms_per_step_with_kernel_events": round(ms_per_step_instr, 5),
+        "kernel_events": ev.kind,
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic", "config": config, "roofline": roof, "cpu_baseline": cpu,
         "per_kernel": per_kernel, "wall_s_timed": round(wall, 4),

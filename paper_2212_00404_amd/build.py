@@ -31,11 +31,16 @@ CFLAGS = [
 ]
 
 
-def source_digest() -> str:
-    """SHA-256 over the kernel and ABI sources (identifies a kernel build)."""
+def source_digest(names=None) -> str:
+    """SHA-256 over kernel sources (identifies a kernel build).  ``names``:
+    file names under ``csrc/`` to cover (default: every source and the ABI
+    header)."""
     import hashlib
     h = hashlib.sha256()
-    files = sorted(glob.glob(os.path.join(CSRC, "*"))) + [os.path.join(INCLUDE, "dconv.h")]
+    if names is None:
+        files = sorted(glob.glob(os.path.join(CSRC, "*"))) + [os.path.join(INCLUDE, "dconv.h")]
+    else:
+        files = [os.path.join(CSRC, n) for n in names]
     for f in files:
         h.update(os.path.basename(f).encode())
         with open(f, "rb") as fh:

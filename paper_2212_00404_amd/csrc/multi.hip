@@ -622,23 +622,29 @@ __global__ __launch_bounds__(256) void multi_generic(const float *__restrict__ I
   O[idx] = acc;
 }
 
-// O[i] = sum_{s < S} ws[s][i], added in the order s = 0, 1, ..., S-1.  The
-// partials are loaded eight at a time so their latencies overlap.
+// O[i] = sum_{s < S} ws[s][i], added in the order s = 0, 1, ..., S-1.  Each
+// thread sums V consecutive outputs (V = 4: 16-byte loads and stores) and
+// issues the loads of up to 16 slots before adding them, so one memory
+// latency covers the common split factors.
+template <int V>
 __global__ __launch_bounds__(256) void split_sum(const float *__restrict__ ws,
                                                  float *__restrict__ O, int64_t n, int S) {
+  typedef float vec __attribute__((ext_vector_type(V)));
+  const int64_t nv = n / V;
   const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= n) return;
-  float acc = 0.f;
-  int s = 0;
-  for (; s + 8 <= S; s += 8) {
-    float v[8];
+  if (i >= nv) return;
+  const vec *src = reinterpret_cast<const vec *>(ws) + i;
+  vec acc = src[0];
+  for (int s0 = 1; s0 < S; s0 += 16) {
+    vec v[16];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) v[j] = ws[(int64_t)(s + j) * n + i];
+    for (int j = 0; j < 16; ++j)
+      if (s0 + j < S) v[j] = src[(int64_t)(s0 + j) * nv];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) acc = (s + j == 0) ? v[j] : acc + v[j];
+    for (int j = 0; j < 16; ++j)
+      if (s0 + j < S) acc += v[j];
   }
-  for (; s < S; ++s) acc = (s == 0) ? ws[i] : acc + ws[(int64_t)s * n + i];
-  O[i] = acc;
+  reinterpret_cast<vec *>(O)[i] = acc;
 }
 
 // Dynamic LDS per workgroup the planner may request (gfx950: 160 KB per CU).
@@ -936,8 +942,14 @@ hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, floa
   }
   if (e != hipSuccess || p.split_c == 1) return e;
   const int64_t n = (int64_t)M * (Wy - p.K + 1) * (Wx - p.K + 1);
-  hipLaunchKernelGGL(split_sum, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, ws, O, n,
-                     p.split_c);
+  // The workspace comes from the device allocator (256-byte aligned); with
+  // n % 4 == 0 every slot starts on a 16-byte boundary.
+  if (n % 4 == 0 && (reinterpret_cast<uintptr_t>(O) & 15) == 0)
+    hipLaunchKernelGGL(split_sum<4>, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, st, ws,
+                       O, n, p.split_c);
+  else
+    hipLaunchKernelGGL(split_sum<1>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, ws, O,
+                       n, p.split_c);
   return hipGetLastError();
 }
 

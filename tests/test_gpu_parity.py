@@ -69,12 +69,16 @@ def test_single_shapes(shape):
 
 # (C, M, Wx, Wy, K): odd channel counts (the MFMA path pairs channels), M not a
 # multiple of any filter tile, K from 1 to beyond the MFMA kernels, tiny and
-# non-square maps, and a filter too large for any LDS tile.
+# non-square maps, a filter too large for any LDS tile, and deep channel
+# sums over tiny maps.
 MULTI_SHAPES = [
     (1, 1, 1, 1, 1), (3, 5, 9, 7, 3), (5, 33, 12, 12, 1), (7, 40, 10, 13, 2), (2, 3, 20, 20, 4),
     (17, 70, 23, 19, 5), (9, 31, 16, 30, 6), (4, 65, 25, 25, 7), (6, 9, 20, 20, 9),
     (3, 4, 17, 21, 11), (2, 3, 40, 40, 31), (33, 129, 15, 15, 3), (64, 64, 7, 7, 7),
     (3, 64, 70, 70, 7), (130, 7, 9, 9, 3), (1, 96, 100, 3, 3),
+    # one or a few outputs per filter and many channels: the channel sum is
+    # split over up to 64 workgroups (vector and scalar split-sum paths)
+    (1024, 32, 3, 3, 3), (1536, 32, 4, 5, 3), (1025, 33, 3, 3, 3),
 ]
 
 
