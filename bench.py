@@ -53,7 +53,73 @@ def parse():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="instead of convolving, copy a MIB-sized device buffer --steps "
                          "times (reference kernel for scaling HBM byte counters)")
+    ap.add_argument("--latency-probe", action="store_true",
+                    help="instead of convolving, measure dependent-load latency over chains of "
+                         "64 KiB to 4 GiB (the latency input of the paper's partition model); "
+                         "one JSON line per footprint and stride")
+    ap.add_argument("--autotune", action="store_true",
+                    help="for the multi-channel workload(s), time every candidate plan, the "
+                         "planner's choice and the paper-rule choice; one JSON line per workload")
     return ap.parse_args()
+
+
+def latency_probe():
+    """dconv_probe_latency over random cyclic chains of growing footprint."""
+    import paper_2212_00404_amd as dc
+    for fp in (1 << 16, 1 << 20, 1 << 22, 1 << 24, 1 << 26, 1 << 28, 1 << 30, 1 << 32):
+        for stride in (256, 4096):
+            print(json.dumps(dc.probe_latency(fp, steps=20000, stride_bytes=stride)), flush=True)
+
+
+def autotune(names, steps, warmup):
+    """Per multi-channel workload: the time of every candidate plan (both
+    kernel families, every workgroup shape and channel split), of the
+    planner's choice and of the plan the paper's Section 3.2 rules pick for
+    an MI355X.  Each plan is timed over `steps` back-to-back launches."""
+    import torch
+    import paper_2212_00404_amd as dc
+    from dconv_workloads import WORKLOADS, make
+    dev = torch.device("cuda:0")
+    for n in names:
+        w = WORKLOADS[n]
+        I, F = make(w)
+        It, Ft = torch.from_numpy(I).to(dev), torch.from_numpy(F).to(dev)
+        Ot = torch.empty((w.M, w.Hout, w.Wout), device=dev)
+        args = (w.C, w.M, w.Wx, w.Wy, w.K)
+
+        def timed(plan):
+            for _ in range(warmup):
+                dc.multi(It, Ft, out=Ot, plan=plan)
+            torch.cuda.synchronize()
+            try:
+                torch.cuda._sleep(int(min(0.2, 6e-5 * steps) * 2.0e9))
+            except (AttributeError, RuntimeError):
+                pass
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(steps):
+                dc.multi(It, Ft, out=Ot, plan=plan)
+            b.record()
+            torch.cuda.synchronize()
+            return a.elapsed_time(b) / steps * 1e3
+
+        def tag(p):
+            fam = "mfma" if p["variant"] == 2 else "valu"
+            return "%s/k%d/m%d/%dx%d/c%d/s%d" % (fam, p["kernel"], p["tile_m"], p["tile_h"],
+                                                p["tile_w"], p["chunk_c"], p["split_c"])
+
+        cands = dc.plan_multi_candidates(*args)
+        times = {tag(p): round(timed(p), 2) for p in cands}
+        best = min(times, key=times.get)
+        planner = tag(dc.plan_multi(*args))
+        paper = tag(dc.plan_multi_paper(*args, dc.MI355X))
+        us = lambda t: times[t]
+        print(json.dumps({
+            "workload": n, "flops": w.flops, "candidates": len(cands),
+            "best": best, "best_us": us(best),
+            "planner": planner, "planner_us": us(planner),
+            "paper_rule": paper, "paper_rule_us": us(paper),
+            "model": dc.model_latency(dc.MI355X), "us": times}), flush=True)
 
 
 def copy_probe(mib, steps):
@@ -234,6 +300,15 @@ def main():
 
     if args.copy_probe:
         copy_probe(args.copy_probe, args.steps)
+        return
+    if args.latency_probe:
+        latency_probe()
+        return
+    if args.autotune:
+        from dconv_workloads import WORKLOADS
+        names = ([args.workload] if args.workload != SWEEP else
+                 [n for n, w in WORKLOADS.items() if w.kind == "multi"])
+        autotune(names, args.steps, args.warmup)
         return
     if args.ingest_pmc:
         data = ingest_pmc(*args.ingest_pmc, copy_mib=512)

@@ -125,6 +125,135 @@ int dconv_plan_single(int Wx, int Wy, int K, int M, int num_cu, dconv_plan *out)
 int dconv_plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_cu,
                      dconv_plan *out);
 
+/*
+ * dconv_plan_multi_candidates -- every plan of a kernel family (both
+ * families for DCONV_VARIANT_AUTO) that fits a device with `num_cu` compute
+ * units: each workgroup shape crossed with each channel split, in a fixed
+ * order.  dconv_plan_multi returns one of them (the planner's estimate is the
+ * smallest).  Writes min(count, capacity) plans to `out` (may be NULL when
+ * capacity is 0) and the total to *count.  For autotuning (Section 3 divides
+ * the work by rules; these are the alternatives the rules choose from).
+ */
+int dconv_plan_multi_candidates(int C, int M, int Wx, int Wy, int K, int variant, int num_cu,
+                                dconv_plan *out, int capacity, int *count);
+
+/*
+ * dconv_multi_with_plan -- dconv_multi with a plan chosen by the caller, which
+ * must equal (field by field) one of the candidates dconv_plan_multi_candidates
+ * returns for these sizes on the current device; DCONV_EINVAL otherwise.
+ * Semantics, workspace and returns as for dconv_multi.
+ */
+int dconv_multi_with_plan(const float *I, const float *F, float *O, int C, int M, int Wx,
+                          int Wy, int K, const dconv_plan *plan, void *stream);
+
+/*
+ * The paper's partition model (host arithmetic only, no device access).
+ *
+ * Section 2.2 and Table 1: to hide a global-memory latency of L clocks a
+ * processor needs N_FMA = L x lanes x (operations per lane per clock) of work
+ * per data set, or the memory must have V_s bytes in flight: the bytes it
+ * delivers per clock (bandwidth / clock, rounded down) times L, fetched one
+ * word per thread (rounded up to whole warps/wavefronts), spread over the
+ * processors and rounded up to whole warps/wavefronts again.  Table 1 (GTX 1080 Ti: L = 258, 484 GB/s, 1480 MHz, 28
+ * SMs of 128 cores, 2 per core per clock, warps of 32, 4-byte words, 96 KB
+ * shared memory) gives N_FMA = 66,048, 327 B/clock, 84,366 B, 21,120
+ * threads, 768 threads = 24 warps = 3,072 B per SM, V_s = 86,016 B.
+ */
+typedef struct dconv_device_params {
+  double latency_clk;    /* global-memory latency, clock cycles */
+  double bandwidth_gbs;  /* memory bandwidth, 1e9 bytes per second */
+  double clock_mhz;      /* the clock the latency is counted in */
+  int num_cu;            /* processors (SMs, compute units) */
+  int lanes_per_cu;      /* arithmetic lanes per processor */
+  int ops_per_clk_lane;  /* per lane per clock, as the paper counts for N_FMA */
+  int wave_size;         /* threads per warp / wavefront */
+  int word_bytes;        /* bytes each thread fetches per load */
+  int onchip_bytes;      /* shared memory / LDS per processor */
+} dconv_device_params;
+
+typedef struct dconv_latency_model {
+  long long n_fma;       /* N_FMA */
+  int bytes_per_clk;     /* transmission rate */
+  long long data_bytes;  /* bytes in flight over one latency */
+  long long threads_total; /* data_bytes / word_bytes, rounded up to whole waves */
+  int threads_per_cu;    /* threads_total / num_cu, rounded up to whole waves */
+  int waves_per_cu;
+  int bytes_per_cu;      /* threads_per_cu x word_bytes */
+  long long v_s;         /* V_s = bytes_per_cu x num_cu */
+} dconv_latency_model;
+
+/* Section 2.2 / Table 1.  DCONV_ENULL, or DCONV_EINVAL if a field is <= 0. */
+int dconv_model_latency(const dconv_device_params *dev, dconv_latency_model *out);
+
+/*
+ * Section 3.1, single-channel division of an Wx x Wy map and M K x K filters
+ * over the processors.  Method 1: filters divided along m, the map streamed
+ * in P pieces along y; on-chip data D1 = (K^2 ceil(M/N) + (ceil(Wy/P)+K-1) Wx)
+ * x word, work Th1 = K^2 ceil(M/N) ceil(Wy/P) Wx.  Method 2: map divided along
+ * y, filters streamed in Q pieces; D2 = (K^2 ceil(M/Q) + (ceil(Wy/N)+K-1) Wx)
+ * x word, Th2 = K^2 ceil(M/Q) ceil(Wy/N) Wx.  P and Q are bounded above by
+ * Th >= N_FMA (and by Wy, M) and below by D <= on-chip bytes; the smallest
+ * admissible value is taken (1 if none), and the method with the smaller D
+ * is kept (the other factor is reset to 1).
+ */
+typedef struct dconv_single_split {
+  int method;                 /* 1 or 2 */
+  int P, Q;                   /* the chosen factors */
+  long long D1, D2;           /* bytes, at the admissible (or unit) P and Q */
+  long long Th1, Th2;         /* multiply-adds per data set */
+  long long p_lo, p_hi;       /* bounds on P (p_lo = -1: on-chip bound unreachable) */
+  long long q_lo, q_hi;       /* bounds on Q */
+  int p_admissible, q_admissible;
+} dconv_single_split;
+
+int dconv_model_single(const dconv_device_params *dev, const dconv_latency_model *lm, int Wx,
+                       int Wy, int K, int M, dconv_single_split *out);
+
+/*
+ * Section 3.2, the stride-fixed block of the multi-channel kernel: a segment
+ * of S bytes of each filter along the channels (S a multiple of the word),
+ * W'x map pixels, W'y = ceil(S / (K x word)) map lines, the smallest M' with
+ * M' x (S / word) x W'x >= N_FMA, and whether the data set
+ * S x M' + W'y x W'x x word fits in half the on-chip memory.
+ */
+typedef struct dconv_multi_block {
+  int S, Wx_p, Wy_p, M_p;
+  long long set_bytes;
+  long long fma_per_set;
+  int fits;
+} dconv_multi_block;
+
+int dconv_model_multi(const dconv_device_params *dev, const dconv_latency_model *lm, int K,
+                      int S, int Wxp, dconv_multi_block *out);
+
+/*
+ * dconv_plan_multi_paper -- the Section 3.2 rules applied to this library's
+ * multi-channel plans for a device described by `dev` (its num_cu and
+ * onchip_bytes included): among the candidates that keep the channel sum
+ * inside a workgroup (the paper does not split it across processors), those
+ * whose stage gives each compute unit at least N_FMA multiply-adds (the
+ * co-resident workgroups, as many as the on-chip memory holds, counted
+ * together); of these the fewest filters per workgroup (smallest M'), then
+ * the most pixels per tile (largest W'x).  If none reaches N_FMA, the
+ * candidate with the most work per compute unit.  For comparison with the
+ * library's own planner and with exhaustive search; `out` can be passed to
+ * dconv_multi_with_plan when dev->num_cu is the device's count.
+ */
+int dconv_plan_multi_paper(int C, int M, int Wx, int Wy, int K, const dconv_device_params *dev,
+                           dconv_plan *out);
+
+/*
+ * dconv_probe_latency -- measure the latency the model above takes as input
+ * (Section 2.2 uses a pointer-chasing measurement).  One lane follows
+ * j <- chain[j] from j = 0 for `steps` dependent loads; the caller's chain
+ * (device memory, every entry a valid index into it) sets the footprint and
+ * so which level of the memory hierarchy is measured.  Writes to the device
+ * array out[3]: elapsed shader clock cycles (s_memtime), elapsed ticks of the
+ * constant 100 MHz counter (s_memrealtime), and the final index.  Enqueued on
+ * `stream`; read `out` after synchronising.
+ */
+int dconv_probe_latency(const int *chain, int steps, long long *out, void *stream);
+
 #ifdef __cplusplus
 }
 #endif

@@ -6,5 +6,6 @@ Maruyama, "Fast convolution kernels on Pascal GPU with high memory
 efficiency" (Section 2.1).  See ``dconv.py`` for the argument conventions and
 ``include/dconv.h`` for the C interface.
 """
-from .dconv import (EXPORTED, Plan, load, multi, plan_multi, plan_single, single,  # noqa: F401
-                    strerror)
+from .dconv import (EXPORTED, GTX_1080TI, MI355X, Plan, load, model_latency,  # noqa: F401
+                    model_multi, model_single, multi, plan_multi, plan_multi_candidates,
+                    plan_multi_paper, plan_single, probe_latency, single, strerror)

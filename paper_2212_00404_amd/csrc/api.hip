@@ -90,22 +90,6 @@ void export_single(const dconv::SinglePlan &p, dconv_plan *out) {
   out->workspace_bytes = 0;
 }
 
-void export_multi(const dconv::MultiPlan &p, dconv_plan *out) {
-  *out = dconv_plan{};
-  out->variant = p.variant;
-  out->kernel = p.kernel;
-  out->tile_m = p.tile_m;
-  out->tile_h = p.tpy;
-  out->tile_w = p.tpx;
-  out->chunk_c = p.chunk_c;
-  out->split_c = p.split_c;
-  out->grid_x = p.grid_x;
-  out->grid_y = p.grid_y;
-  out->grid_z = p.grid_z;
-  out->block = p.block;
-  out->lds_bytes = p.lds_bytes;
-  out->workspace_bytes = p.workspace_bytes;
-}
 
 }  // namespace
 
@@ -122,19 +106,12 @@ DCONV_EXPORT int dconv_single(const float *I, const float *F, float *O, int Wx, 
   return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
 }
 
-DCONV_EXPORT int dconv_multi_variant(const float *I, const float *F, float *O, int C, int M,
-                                     int Wx, int Wy, int K, int variant, void *stream) {
-  if (!I || !F || !O) return DCONV_ENULL;
-  if (variant != DCONV_VARIANT_AUTO && variant != DCONV_VARIANT_VALU &&
-      variant != DCONV_VARIANT_MFMA)
-    return DCONV_EINVAL;
-  int rc = validate_sizes(C, M, Wx, Wy, K);
-  if (rc != DCONV_OK) return rc;
-  int num_cu = 0;
-  if ((rc = current_num_cu(&num_cu)) != DCONV_OK) return rc;
-  dconv::MultiPlan p;
-  if ((rc = dconv::plan_multi(C, M, Wx, Wy, K, variant, num_cu, &p)) != DCONV_OK) return rc;
-  hipStream_t st = (hipStream_t)stream;
+namespace {
+
+// Launch a multi-channel plan, with the stream's workspace when it splits
+// the channel sum.
+int run_multi(const dconv::MultiPlan &p, const float *I, const float *F, float *O, int C, int M,
+              int Wx, int Wy, hipStream_t st) {
   if (p.workspace_bytes == 0) {
     const hipError_t e = dconv::launch_multi(p, I, F, O, nullptr, C, M, Wx, Wy, st);
     return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
@@ -166,6 +143,68 @@ DCONV_EXPORT int dconv_multi_variant(const float *I, const float *F, float *O, i
   return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
 }
 
+bool same_plan(const dconv_plan &a, const dconv_plan &b) {
+  return a.variant == b.variant && a.kernel == b.kernel && a.tile_m == b.tile_m &&
+         a.tile_h == b.tile_h && a.tile_w == b.tile_w && a.chunk_c == b.chunk_c &&
+         a.split_c == b.split_c && a.grid_x == b.grid_x && a.grid_y == b.grid_y &&
+         a.grid_z == b.grid_z && a.block == b.block && a.lds_bytes == b.lds_bytes &&
+         a.workspace_bytes == b.workspace_bytes;
+}
+
+}  // namespace
+
+DCONV_EXPORT int dconv_multi_variant(const float *I, const float *F, float *O, int C, int M,
+                                     int Wx, int Wy, int K, int variant, void *stream) {
+  if (!I || !F || !O) return DCONV_ENULL;
+  if (variant != DCONV_VARIANT_AUTO && variant != DCONV_VARIANT_VALU &&
+      variant != DCONV_VARIANT_MFMA)
+    return DCONV_EINVAL;
+  int rc = validate_sizes(C, M, Wx, Wy, K);
+  if (rc != DCONV_OK) return rc;
+  int num_cu = 0;
+  if ((rc = current_num_cu(&num_cu)) != DCONV_OK) return rc;
+  dconv::MultiPlan p;
+  if ((rc = dconv::plan_multi(C, M, Wx, Wy, K, variant, num_cu, &p)) != DCONV_OK) return rc;
+  return run_multi(p, I, F, O, C, M, Wx, Wy, (hipStream_t)stream);
+}
+
+DCONV_EXPORT int dconv_multi_with_plan(const float *I, const float *F, float *O, int C, int M,
+                                       int Wx, int Wy, int K, const dconv_plan *plan,
+                                       void *stream) {
+  if (!I || !F || !O || !plan) return DCONV_ENULL;
+  int rc = validate_sizes(C, M, Wx, Wy, K);
+  if (rc != DCONV_OK) return rc;
+  int num_cu = 0;
+  if ((rc = current_num_cu(&num_cu)) != DCONV_OK) return rc;
+  std::vector<dconv::MultiPlan> all;
+  if (dconv::multi_candidates(C, M, Wx, Wy, K, DCONV_VARIANT_AUTO, num_cu, all) != DCONV_OK)
+    return DCONV_EINVAL;
+  for (const auto &p : all) {
+    dconv_plan e;
+    dconv::export_multi_plan(p, &e);
+    if (same_plan(e, *plan)) return run_multi(p, I, F, O, C, M, Wx, Wy, (hipStream_t)stream);
+  }
+  return DCONV_EINVAL;
+}
+
+DCONV_EXPORT int dconv_plan_multi_candidates(int C, int M, int Wx, int Wy, int K, int variant,
+                                             int num_cu, dconv_plan *out, int capacity,
+                                             int *count) {
+  if (!count || (capacity > 0 && !out)) return DCONV_ENULL;
+  if (capacity < 0) return DCONV_EINVAL;
+  if (variant != DCONV_VARIANT_AUTO && variant != DCONV_VARIANT_VALU &&
+      variant != DCONV_VARIANT_MFMA)
+    return DCONV_EINVAL;
+  int rc = validate_sizes(C, M, Wx, Wy, K);
+  if (rc != DCONV_OK) return rc;
+  std::vector<dconv::MultiPlan> all;
+  rc = dconv::multi_candidates(C, M, Wx, Wy, K, variant, num_cu, all);
+  *count = (int)all.size();
+  if (rc != DCONV_OK) return rc;
+  for (int i = 0; i < capacity && i < (int)all.size(); ++i) dconv::export_multi_plan(all[i], out + i);
+  return DCONV_OK;
+}
+
 DCONV_EXPORT int dconv_multi(const float *I, const float *F, float *O, int C, int M, int Wx,
                              int Wy, int K, void *stream) {
   return dconv_multi_variant(I, F, O, C, M, Wx, Wy, K, DCONV_VARIANT_AUTO, stream);
@@ -175,7 +214,9 @@ DCONV_EXPORT const char *dconv_strerror(int status) {
   switch (status) {
     case DCONV_OK: return "success";
     case DCONV_ENULL: return "a required pointer is NULL";
-    case DCONV_EINVAL: return "invalid size or variant (need C, M, K >= 1 and K <= min(Wx, Wy))";
+    case DCONV_EINVAL:
+      return "invalid size, variant or plan (need C, M, K >= 1 and K <= min(Wx, Wy); a plan "
+             "must be one of the candidates for these sizes)";
     case DCONV_ERANGE: return "a tensor has more than 2^31-1 elements";
     case DCONV_EHIP: return "the HIP runtime reported an error";
     case DCONV_EUNSUPPORTED: return "the requested kernel family cannot run this shape";
@@ -206,6 +247,6 @@ DCONV_EXPORT int dconv_plan_multi(int C, int M, int Wx, int Wy, int K, int varia
   if ((rc = dconv::plan_multi(C, M, Wx, Wy, K, variant, num_cu > 0 ? num_cu : 256, &p)) !=
       DCONV_OK)
     return rc;
-  export_multi(p, out);
+  dconv::export_multi_plan(p, out);
   return DCONV_OK;
 }

@@ -4,6 +4,7 @@
 
 #include <hip/hip_runtime.h>
 #include <cstdint>
+#include <vector>
 
 #include "dconv.h"
 
@@ -65,6 +66,12 @@ struct MultiPlan {
 };
 
 int plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_cu, MultiPlan *p);
+// Every plan of the family (or both families for DCONV_VARIANT_AUTO) that
+// fits the device, in a fixed order; plan_multi picks one of them.
+int multi_candidates(int C, int M, int Wx, int Wy, int K, int variant, int num_cu,
+                     std::vector<MultiPlan> &out);
+// The public description of a plan.
+void export_multi_plan(const MultiPlan &p, dconv_plan *out);
 hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, float *O,
                         float *ws, int C, int M, int Wx, int Wy, hipStream_t s);
 

@@ -30,6 +30,9 @@
 //   * VALU: one output pixel per lane and MR filters per wave, with the
 //     filter values wave-uniform in scalar registers and one fp32 FMA per
 //     term (packed fp32 FMAs are not used).
+#include <utility>
+#include <vector>
+
 #include "internal.h"
 
 namespace dconv {
@@ -807,11 +810,12 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, i
   return (work > chain ? work : chain) + latency + 2000.0 + extra;
 }
 
-int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, MultiPlan *best) {
+// Every (shape, channel split) of one family whose LDS footprint fits, with
+// the time model's estimate, in a fixed order (shape, then split).
+void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu,
+                      std::vector<std::pair<double, MultiPlan>> &out) {
   const int Hout = Wy - K + 1, Wout = Wx - K + 1;
-  double best_t = 1e300;
   const int n = mfma ? kNumMfma : kNumValu;
-  bool found = false;
   for (int i = 0; i < n; ++i) {
     const Candidate cd = mfma ? mfma_candidate(i, K) : valu_candidate(i);
     const TileChoice t = choose_tile(Hout, Wout, cd.PT);
@@ -829,32 +833,28 @@ int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, Mult
       const int real_split = (C + cps - 1) / cps;
       if (real_split != split) break;
       const double tm = estimate(cd, mfma, C, M, K, Hout, Wout, num_cu, t, split, cps, lds_bytes);
-      if (tm < best_t) {
-        best_t = tm;
-        found = true;
-        MultiPlan p{};
-        p.variant = mfma ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
-        p.kernel = i;
-        p.K = K;
-        p.tile_m = cd.MT;
-        p.tpy = t.tpy;
-        p.tpx = t.tpx;
-        p.tiles_x = t.tiles_x;
-        p.tiles_y = t.tiles_y;
-        p.chunk_c = cd.CC;
-        p.split_c = split;
-        p.c_per_split = cps;
-        p.grid_x = (int)((int64_t)t.tiles_x * t.tiles_y * ((M + cd.MT - 1) / cd.MT) * split);
-        p.grid_y = 1;
-        p.grid_z = 1;
-        p.block = kBlock;
-        p.lds_bytes = (int)lds_bytes;
-        p.workspace_bytes = split > 1 ? (int64_t)split * M * Hout * Wout * 4 : 0;
-        *best = p;
-      }
+      MultiPlan p{};
+      p.variant = mfma ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
+      p.kernel = i;
+      p.K = K;
+      p.tile_m = cd.MT;
+      p.tpy = t.tpy;
+      p.tpx = t.tpx;
+      p.tiles_x = t.tiles_x;
+      p.tiles_y = t.tiles_y;
+      p.chunk_c = cd.CC;
+      p.split_c = split;
+      p.c_per_split = cps;
+      p.grid_x = (int)((int64_t)t.tiles_x * t.tiles_y * ((M + cd.MT - 1) / cd.MT) * split);
+      p.grid_y = 1;
+      p.grid_z = 1;
+      p.block = kBlock;
+      p.lds_bytes = (int)lds_bytes;
+      p.workspace_bytes = split > 1 ? (int64_t)split * M * Hout * Wout * 4 : 0;
+      out.emplace_back(tm, p);
     }
   }
-  if (!found && !mfma) {
+  if (out.empty() && !mfma) {
     // No tiled shape fits in LDS: one output per thread from the caches.
     const int64_t total = (int64_t)M * Hout * Wout;
     MultiPlan p{};
@@ -874,10 +874,19 @@ int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, Mult
     p.block = 256;
     p.lds_bytes = 0;
     p.workspace_bytes = 0;
-    *best = p;
-    found = true;
+    out.emplace_back(0.0, p);
   }
-  return found ? DCONV_OK : DCONV_EUNSUPPORTED;
+}
+
+int plan_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu, MultiPlan *best) {
+  std::vector<std::pair<double, MultiPlan>> all;
+  enumerate_family(C, M, Wx, Wy, K, mfma, num_cu, all);
+  if (all.empty()) return DCONV_EUNSUPPORTED;
+  size_t b = 0;
+  for (size_t k = 1; k < all.size(); ++k)
+    if (all[k].first < all[b].first) b = k;
+  *best = all[b].second;
+  return DCONV_OK;
 }
 
 }  // namespace
@@ -893,6 +902,36 @@ int plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_cu, Mul
   // vector FMAs, so they are preferred wherever a kernel exists.
   if (K <= kMfmaMaxK && plan_family(C, M, Wx, Wy, K, true, num_cu, p) == DCONV_OK) return DCONV_OK;
   return plan_family(C, M, Wx, Wy, K, false, num_cu, p);
+}
+
+void export_multi_plan(const MultiPlan &p, dconv_plan *out) {
+  *out = dconv_plan{};
+  out->variant = p.variant;
+  out->kernel = p.kernel;
+  out->tile_m = p.tile_m;
+  out->tile_h = p.tpy;
+  out->tile_w = p.tpx;
+  out->chunk_c = p.chunk_c;
+  out->split_c = p.split_c;
+  out->grid_x = p.grid_x;
+  out->grid_y = p.grid_y;
+  out->grid_z = p.grid_z;
+  out->block = p.block;
+  out->lds_bytes = p.lds_bytes;
+  out->workspace_bytes = p.workspace_bytes;
+}
+
+int multi_candidates(int C, int M, int Wx, int Wy, int K, int variant, int num_cu,
+                     std::vector<MultiPlan> &out) {
+  if (num_cu <= 0) num_cu = 256;
+  std::vector<std::pair<double, MultiPlan>> all;
+  if ((variant == DCONV_VARIANT_AUTO || variant == DCONV_VARIANT_MFMA) && K <= kMfmaMaxK)
+    enumerate_family(C, M, Wx, Wy, K, true, num_cu, all);
+  if (variant == DCONV_VARIANT_AUTO || variant == DCONV_VARIANT_VALU)
+    enumerate_family(C, M, Wx, Wy, K, false, num_cu, all);
+  out.clear();
+  for (const auto &e : all) out.push_back(e.second);
+  return out.empty() ? DCONV_EUNSUPPORTED : DCONV_OK;
 }
 
 hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, float *O, float *ws,
