@@ -30,9 +30,12 @@ PEAK_FP32_UNPACKED_TFLOPS = 78.6     # one fp32 FMA per lane per clock
 PEAK_FP32_MFMA_TFLOPS = 157.3
 PEAK_HBM_GBS = 8000.0
 SWEEP = "single_4096x4096_m1_k3-11"
+# Named multi-launch steps: the default sweep, single-map layers with many
+# filters, and the multi-channel layers.
+SWEEPS = ("single_4096x4096_m1_k3-11", "single_multi_filter", "multi_layers")
 # Sources the single-map kernels are built from: recorded HBM traffic stays
 # valid while these are unchanged.
-SINGLE_SOURCES = ("single.hip", "internal.h")
+SINGLE_SOURCES = ("single.hip", "xcd.h")
 
 
 def parse():
@@ -41,7 +44,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=SWEEP,
-                    help="%s (default) or a name from dconv_workloads.WORKLOADS" % SWEEP)
+                    help="%s (default), %s, %s, or a name from dconv_workloads.WORKLOADS"
+                         % SWEEPS)
     ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "valu"],
                     help="kernel family for multi-channel workloads")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -201,25 +205,30 @@ def traffic_for(kernel_tag):
     return ent.get("bytes_per_launch")
 
 
-def cpu_baseline(launches, reps):
-    """The fp64 oracle on the host cores over the same launches (whole step)."""
+def cpu_baseline(launches, reps, min_seconds=10.0):
+    """The fp64 oracle on the host cores over the same launches: whole steps,
+    repeated at least `reps` times and until `min_seconds` of CPU work have
+    run; the rate of the fastest step is reported."""
     import oracle
     threads = int(os.environ.get("OMP_NUM_THREADS") or 0) or oracle.default_threads()
     flops = sum(w.flops for w, _, _ in launches)
-    best = None
-    for _ in range(max(1, reps)):
+    times = []
+    t_start = time.perf_counter()
+    while len(times) < max(1, reps) or time.perf_counter() - t_start < min_seconds:
         t0 = time.perf_counter()
         for w, I, F in launches:
             if w.kind == "single":
                 oracle.conv_single(I, F, threads=threads)
             else:
                 oracle.conv_multi(I, F, threads=threads)
-        dt = time.perf_counter() - t0
-        best = dt if best is None else min(best, dt)
+        times.append(time.perf_counter() - t0)
+    best = min(times)
     return {"value": round(flops / best / 1e9, 3), "unit": "GFLOP/s", "cores": threads,
             "kind": "oracle",
-            "sample": "one full step (%d launch%s, %.2f GFLOP), best of %d, fp64 C oracle"
-                      % (len(launches), "es" if len(launches) > 1 else "", flops / 1e9, reps)}
+            "sample": "whole steps (%d launch%s, %.2f GFLOP each), %d repetitions in %.1f s, "
+                      "fastest reported, fp64 C oracle"
+                      % (len(launches), "es" if len(launches) > 1 else "", flops / 1e9,
+                         len(times), sum(times))}
 
 
 class KernelEvents:
@@ -306,7 +315,7 @@ def main():
         return
     if args.autotune:
         from dconv_workloads import WORKLOADS
-        names = ([args.workload] if args.workload != SWEEP else
+        names = ([args.workload] if args.workload not in SWEEPS else
                  [n for n, w in WORKLOADS.items() if w.kind == "multi"])
         autotune(names, args.steps, args.warmup)
         return
@@ -320,9 +329,11 @@ def main():
 
     import torch
     import paper_2212_00404_amd as dc
-    from dconv_workloads import SINGLE_4096_SWEEP, WORKLOADS, make
+    from dconv_workloads import SINGLE_4096_SWEEP, SINGLE_MULTI_FILTER, WORKLOADS, make
 
-    names = list(SINGLE_4096_SWEEP) if args.workload == SWEEP else [args.workload]
+    sweeps = {SWEEP: list(SINGLE_4096_SWEEP), "single_multi_filter": list(SINGLE_MULTI_FILTER),
+              "multi_layers": [n for n, w in WORKLOADS.items() if w.kind == "multi"]}
+    names = sweeps.get(args.workload, [args.workload])
     for n in names:
         if n not in WORKLOADS:
             sys.exit("unknown workload %s" % n)
@@ -450,6 +461,10 @@ def main():
         config = {"workload": SWEEP, "kind": "single", "Wx": 4096, "Wy": 4096, "M": 1, "C": 1,
                   "K": [3, 5, 7, 9, 11], "launches_per_step": 5,
                   "buffers": "separate I/O per K (670 MB per step)"}
+    elif args.workload in sweeps:
+        config = {"workload": args.workload, "kind": bufs[0][0].kind,
+                  "workloads": [b[0].name for b in bufs], "variant": args.variant,
+                  "launches_per_step": len(bufs)}
     else:
         config = {"workload": w.name, "kind": w.kind, "C": w.C, "M": w.M, "Wx": w.Wx,
                   "Wy": w.Wy, "K": w.K, "variant": args.variant, "launches_per_step": 1}

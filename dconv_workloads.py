@@ -7,7 +7,8 @@ recipes.
 
 Workloads mirror the layer shapes the paper evaluates (Section 4: CNN
 convolution layers with feature maps from 7 to 1K pixels, 64 to 512 channels
-and filter sizes 1, 3, 5) plus a large single-map case with K up to 11.  The
+and filter sizes 1, 3, 5; single-channel layers with 32 to 512 filters) plus
+a large single-map case with K up to 11.  The
 paper used no dataset, only layer shapes, so seeded synthetic data stands in:
 
 * single-map workloads: input and filters uniform in [-1, 1);
@@ -84,10 +85,22 @@ WORKLOADS = {w.name: w for w in [
     _multi("multi_c64_114x114_m128_k3", 64, 114, 128, 3),
     _multi("multi_c128_60x60_m128_k5", 128, 60, 128, 5),
     _multi("multi_c256_28x28_m256_k1", 256, 28, 256, 1),
+    # one input map, many filters: the single-channel layers the paper
+    # targets (maps of 28 to 1K pixels, 32 to 512 filters, K = 1, 3, 5)
+    _single("single_28x28_m512_k3", 28, 512, 3),
+    _single("single_56x56_m256_k5", 56, 256, 5),
+    _single("single_112x112_m128_k3", 112, 128, 3),
+    _single("single_224x224_m64_k5", 224, 64, 5),
+    _single("single_512x512_m128_k1", 512, 128, 1),
+    _single("single_1024x1024_m32_k3", 1024, 32, 3),
 ]}
 
 # The large single-map workload is one pass over all five filter sizes.
 SINGLE_4096_SWEEP = tuple("single_4096x4096_m1_k%d" % k for k in (3, 5, 7, 9, 11))
+# Single map, many filters.
+SINGLE_MULTI_FILTER = ("single_28x28_m512_k3", "single_56x56_m256_k5", "single_112x112_m128_k3",
+                       "single_224x224_m64_k5", "single_512x512_m128_k1",
+                       "single_1024x1024_m32_k3")
 
 
 def make(w: Workload | str, variant: str = "float", seed: int | None = None):
