@@ -32,7 +32,7 @@ PEAK_HBM_GBS = 8000.0
 SWEEP = "single_4096x4096_m1_k3-11"
 # Named multi-launch steps: the default sweep, single-map layers with many
 # filters, and the multi-channel layers.
-SWEEPS = ("single_4096x4096_m1_k3-11", "single_multi_filter", "multi_layers")
+SWEEPS = ("single_4096x4096_m1_k3-11", "single_multi_filter", "multi_layers", "paper_multi_sweep")
 # Sources the single-map kernels are built from: recorded HBM traffic stays
 # valid while these are unchanged.
 SINGLE_SOURCES = ("single.hip", "xcd.h")
@@ -44,7 +44,7 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=SWEEP,
-                    help="%s (default), %s, %s, or a name from dconv_workloads.WORKLOADS"
+                    help="%s (default), %s, %s, %s, or a name from dconv_workloads.WORKLOADS"
                          % SWEEPS)
     ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "valu"],
                     help="kernel family for multi-channel workloads")
@@ -61,6 +61,10 @@ def parse():
                     help="instead of convolving, measure dependent-load latency over chains of "
                          "64 KiB to 4 GiB (the latency input of the paper's partition model); "
                          "one JSON line per footprint and stride")
+    ap.add_argument("--miopen", action="store_true",
+                    help="also time torch.nn.functional.conv2d (MIOpen on ROCm, fp32 with "
+                         "TF32 disabled) on each multi-channel workload of the step, as "
+                         "context beside each kernel's time")
     ap.add_argument("--autotune", action="store_true",
                     help="for the multi-channel workload(s), time every candidate plan, the "
                          "planner's choice and the paper-rule choice; one JSON line per workload")
@@ -231,6 +235,36 @@ def cpu_baseline(launches, reps, min_seconds=10.0):
                          len(times), sum(times))}
 
 
+def miopen_context(bufs, per_kernel, steps, warmup):
+    """torch's own convolution (MIOpen) on the same inputs: a context figure
+    for each multi-channel workload, not a parity reference.  Eq. 1 is what
+    conv2d computes with no padding, stride 1 and weights [M][C][K][K]."""
+    import torch
+    torch.backends.cudnn.allow_tf32 = False
+    torch.backends.cuda.matmul.allow_tf32 = False
+    for i, (w, It, Ft, Ot) in enumerate(bufs):
+        if w.kind != "multi":
+            continue
+        x = It[None]
+        ref = None
+        for _ in range(max(warmup, 3)):
+            ref = torch.nn.functional.conv2d(x, Ft)
+        torch.cuda.synchronize()
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(steps):
+            torch.nn.functional.conv2d(x, Ft)
+        b.record()
+        torch.cuda.synchronize()
+        us = a.elapsed_time(b) / steps * 1e3
+        diff = (ref[0] - Ot).abs().max().item()
+        scale = Ot.abs().max().item() or 1.0
+        per_kernel[i]["miopen_us"] = round(us, 2)
+        per_kernel[i]["miopen_tflops"] = round(w.flops / (us * 1e-6) / 1e12, 2)
+        per_kernel[i]["dconv_speedup_vs_miopen"] = round(us / per_kernel[i]["avg_us"], 3)
+        per_kernel[i]["miopen_max_rel_diff"] = float("%.3g" % (diff / scale))
+
+
 class KernelEvents:
     """HIP event pairs around each launch of the instrumented pass.
 
@@ -315,8 +349,9 @@ def main():
         return
     if args.autotune:
         from dconv_workloads import WORKLOADS
-        names = ([args.workload] if args.workload not in SWEEPS else
-                 [n for n, w in WORKLOADS.items() if w.kind == "multi"])
+        from dconv_workloads import MULTI_CONFIGS, PAPER_MULTI_SWEEP
+        names = {"paper_multi_sweep": list(PAPER_MULTI_SWEEP)}.get(
+            args.workload, [args.workload] if args.workload not in SWEEPS else list(MULTI_CONFIGS))
         autotune(names, args.steps, args.warmup)
         return
     if args.ingest_pmc:
@@ -329,10 +364,11 @@ def main():
 
     import torch
     import paper_2212_00404_amd as dc
-    from dconv_workloads import SINGLE_4096_SWEEP, SINGLE_MULTI_FILTER, WORKLOADS, make
+    from dconv_workloads import (MULTI_CONFIGS, PAPER_MULTI_SWEEP, SINGLE_4096_SWEEP,
+                                 SINGLE_MULTI_FILTER, WORKLOADS, make)
 
     sweeps = {SWEEP: list(SINGLE_4096_SWEEP), "single_multi_filter": list(SINGLE_MULTI_FILTER),
-              "multi_layers": [n for n, w in WORKLOADS.items() if w.kind == "multi"]}
+              "multi_layers": list(MULTI_CONFIGS), "paper_multi_sweep": list(PAPER_MULTI_SWEEP)}
     names = sweeps.get(args.workload, [args.workload])
     for n in names:
         if n not in WORKLOADS:
@@ -429,6 +465,9 @@ def main():
             "tflops": round(tf, 2), "gbs": round(gbs, 1), "flop_per_byte": round(ai, 2),
             "frac_fp32_peak": round(tf / PEAK_FP32_VECTOR_TFLOPS, 4),
             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
+
+    if args.miopen:
+        miopen_context(bufs, per_kernel, args.steps, args.warmup)
 
     dom = max(range(len(bufs)), key=lambda i: per_kernel[i]["avg_us"])
     w = bufs[dom][0]

@@ -93,10 +93,22 @@ WORKLOADS = {w.name: w for w in [
     _single("single_224x224_m64_k5", 224, 64, 5),
     _single("single_512x512_m128_k1", 512, 128, 1),
     _single("single_1024x1024_m32_k3", 1024, 32, 3),
+    # the paper's multi-channel sweep (Section 4: maps 7 to 512, 64 to 512
+    # channels, K = 1, 3, 5), as CNN-layer-like shapes with C = M
+    *[_multi("layer_c%d_%dx%d_m%d_k%d" % (c, w, w, c, k), c, w, c, k) for c, w, k in (
+        (64, 512, 3), (64, 224, 3), (128, 112, 3), (256, 56, 3), (512, 28, 3), (512, 14, 3),
+        (512, 7, 3), (64, 56, 1), (256, 28, 1), (512, 14, 1), (64, 56, 5), (128, 28, 5),
+        (256, 14, 5))],
 ]}
 
 # The large single-map workload is one pass over all five filter sizes.
 SINGLE_4096_SWEEP = tuple("single_4096x4096_m1_k%d" % k for k in (3, 5, 7, 9, 11))
+# The multi-channel configurations.
+MULTI_CONFIGS = ("multi_c512_9x9_m512_k3", "multi_c256_30x30_m256_k3", "multi_c512_16x16_m512_k3",
+                 "multi_c64_114x114_m128_k3", "multi_c128_60x60_m128_k5",
+                 "multi_c256_28x28_m256_k1")
+# The paper's multi-channel layer sweep.
+PAPER_MULTI_SWEEP = tuple(n for n in WORKLOADS if n.startswith("layer_"))
 # Single map, many filters.
 SINGLE_MULTI_FILTER = ("single_28x28_m512_k3", "single_56x56_m256_k5", "single_112x112_m128_k3",
                        "single_224x224_m64_k5", "single_512x512_m128_k1",
