@@ -52,7 +52,7 @@ extern "C" {
 #define DCONV_EUNSUPPORTED (-5) /* the forced variant cannot run this shape */
 #define DCONV_ENOMEM (-6)       /* a stream-ordered workspace could not be allocated */
 
-/* Kernel families for dconv_multi_variant / dconv_plan_multi. */
+/* Kernel families for the *_variant calls and the plans. */
 #define DCONV_VARIANT_AUTO 0 /* the planner's choice */
 #define DCONV_VARIANT_VALU 1 /* direct convolution on the fp32 vector FMA units */
 #define DCONV_VARIANT_MFMA 2 /* implicit GEMM over C*K*K on the fp32 matrix cores */
@@ -68,6 +68,18 @@ extern "C" {
  */
 int dconv_single(const float *I, const float *F, float *O, int Wx, int Wy, int K,
                  int M, void *stream);
+
+/*
+ * dconv_single_variant -- dconv_single with the kernel family forced:
+ * DCONV_VARIANT_VALU (vector FMAs), DCONV_VARIANT_MFMA (the fp32 matrix
+ * cores on a banded form of each filter row) or DCONV_VARIANT_AUTO (the
+ * planner's choice, what dconv_single does).  DCONV_EUNSUPPORTED if the
+ * matrix-core family is forced where it has no kernel (K < 5, K > 11, or an
+ * input whose rows are not 16-byte aligned: I not 16-byte aligned or Wx not
+ * a multiple of 4).  Other returns as for dconv_single.
+ */
+int dconv_single_variant(const float *I, const float *F, float *O, int Wx, int Wy, int K,
+                         int M, int variant, void *stream);
 
 /*
  * dconv_multi -- Eq. 1: C input maps, M filters of C channels each.
@@ -122,6 +134,9 @@ typedef struct dconv_plan {
  * Validation is the same as for the compute calls.  `out` must not be NULL.
  */
 int dconv_plan_single(int Wx, int Wy, int K, int M, int num_cu, dconv_plan *out);
+/* The plan dconv_single_variant would use (the input assumed 16-byte aligned). */
+int dconv_plan_single_variant(int Wx, int Wy, int K, int M, int variant, int num_cu,
+                              dconv_plan *out);
 int dconv_plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_cu,
                      dconv_plan *out);
 

@@ -27,6 +27,9 @@ CFLAGS = [
     "--offload-arch=" + ARCH, "-O3", "-std=c++17", "-fPIC", "-fvisibility=hidden",
     "-Wall", "-Wno-unused-function",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    # fully unroll the long compile-time loops of the matrix-core single-map
+    # kernel (its register arrays are indexed by the loop counters)
+    "-mllvm", "-pragma-unroll-threshold=1000000",
     "-I" + INCLUDE, "-I" + CSRC,
 ]
 

@@ -75,7 +75,7 @@ int validate_sizes(int C, int M, int Wx, int Wy, int K) {
 
 void export_single(const dconv::SinglePlan &p, dconv_plan *out) {
   *out = dconv_plan{};
-  out->variant = DCONV_VARIANT_VALU;
+  out->variant = p.kernel == 3 ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
   out->kernel = p.kernel;
   out->tile_m = p.m_per_block;
   out->tile_h = p.tile_h;
@@ -93,17 +93,27 @@ void export_single(const dconv::SinglePlan &p, dconv_plan *out) {
 
 }  // namespace
 
-DCONV_EXPORT int dconv_single(const float *I, const float *F, float *O, int Wx, int Wy, int K,
-                              int M, void *stream) {
+DCONV_EXPORT int dconv_single_variant(const float *I, const float *F, float *O, int Wx, int Wy,
+                                      int K, int M, int variant, void *stream) {
   if (!I || !F || !O) return DCONV_ENULL;
+  if (variant != DCONV_VARIANT_AUTO && variant != DCONV_VARIANT_VALU &&
+      variant != DCONV_VARIANT_MFMA)
+    return DCONV_EINVAL;
   int rc = validate_sizes(1, M, Wx, Wy, K);
   if (rc != DCONV_OK) return rc;
   int num_cu = 0;
   if ((rc = current_num_cu(&num_cu)) != DCONV_OK) return rc;
   dconv::SinglePlan p;
-  dconv::plan_single(Wx, Wy, K, M, num_cu, (reinterpret_cast<uintptr_t>(I) & 15) == 0, &p);
+  rc = dconv::plan_single(Wx, Wy, K, M, num_cu, (reinterpret_cast<uintptr_t>(I) & 15) == 0,
+                          variant, &p);
+  if (rc != DCONV_OK) return rc;
   const hipError_t e = dconv::launch_single(p, I, F, O, Wx, Wy, M, (hipStream_t)stream);
   return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
+}
+
+DCONV_EXPORT int dconv_single(const float *I, const float *F, float *O, int Wx, int Wy, int K,
+                              int M, void *stream) {
+  return dconv_single_variant(I, F, O, Wx, Wy, K, M, DCONV_VARIANT_AUTO, stream);
 }
 
 namespace {
@@ -225,14 +235,23 @@ DCONV_EXPORT const char *dconv_strerror(int status) {
   }
 }
 
-DCONV_EXPORT int dconv_plan_single(int Wx, int Wy, int K, int M, int num_cu, dconv_plan *out) {
+DCONV_EXPORT int dconv_plan_single_variant(int Wx, int Wy, int K, int M, int variant,
+                                           int num_cu, dconv_plan *out) {
   if (!out) return DCONV_ENULL;
-  const int rc = validate_sizes(1, M, Wx, Wy, K);
+  if (variant != DCONV_VARIANT_AUTO && variant != DCONV_VARIANT_VALU &&
+      variant != DCONV_VARIANT_MFMA)
+    return DCONV_EINVAL;
+  int rc = validate_sizes(1, M, Wx, Wy, K);
   if (rc != DCONV_OK) return rc;
   dconv::SinglePlan p;
-  dconv::plan_single(Wx, Wy, K, M, num_cu > 0 ? num_cu : 256, true, &p);
+  rc = dconv::plan_single(Wx, Wy, K, M, num_cu > 0 ? num_cu : 256, true, variant, &p);
+  if (rc != DCONV_OK) return rc;
   export_single(p, out);
   return DCONV_OK;
+}
+
+DCONV_EXPORT int dconv_plan_single(int Wx, int Wy, int K, int M, int num_cu, dconv_plan *out) {
+  return dconv_plan_single_variant(Wx, Wy, K, M, DCONV_VARIANT_AUTO, num_cu, out);
 }
 
 DCONV_EXPORT int dconv_plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_cu,

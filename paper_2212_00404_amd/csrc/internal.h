@@ -15,7 +15,7 @@ namespace dconv {
 // Single-map kernels (Eq. 2)
 // ---------------------------------------------------------------------------
 struct SinglePlan {
-  int kernel;     // 0: tiled (float4 rows), 1: generic, 2: tiled (unaligned rows)
+  int kernel;     // 0: tiled (float4 rows), 1: generic, 2: tiled (unaligned rows), 3: matrix cores
   int K;
   int rows;       // output rows per lane (R)
   int tile_h, tile_w;
@@ -31,7 +31,11 @@ constexpr int kMaxTiledK = 11;
 
 // aligned: the input map pointer is 16-byte aligned (with Wx % 4 == 0 the
 // tiled kernel then stages whole float4).
-void plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, SinglePlan *p);
+// variant: DCONV_VARIANT_AUTO / _VALU / _MFMA; DCONV_EUNSUPPORTED if the
+// matrix-core kernel is forced where it has no instance (K < 5 or K > 11,
+// or rows not 16-byte aligned).
+int plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, int variant,
+                SinglePlan *p);
 hipError_t launch_single(const SinglePlan &p, const float *I, const float *F, float *O,
                          int Wx, int Wy, int M, hipStream_t s);
 

@@ -65,7 +65,8 @@ struct TileShape {
   static constexpr int IH = TH + K - 1;            // staged input rows
   static constexpr int NQ = (kW + K - 1 + 3) / 4;  // float4 reads per lane per row
   static constexpr int IW4 = kLanes + NQ - 1;      // float4 per staged row
-  static constexpr int LDS = IH * IW4 * 16;
+  static constexpr int LW4 = IW4;                  // LDS stride of a staged row (float4)
+  static constexpr int LDS = IH * LW4 * 16;
 };
 
 // Barrier for LDS hand-over inside a workgroup.  Unlike __syncthreads() it
@@ -78,11 +79,12 @@ __device__ __forceinline__ void lds_barrier() {
 // Loads of one staged tile held in registers between fetch() and commit().
 // VEC4: every map row starts on a 16-byte boundary, so whole float4 are
 // loaded; otherwise single floats.  Values outside the map are zero.
-template <int K, int R, bool VEC4>
+// S: the tile shape (IH staged rows of IW4 float4, stored LW4 float4 apart).
+template <class S, bool VEC4>
 struct Stager {
-  using S = TileShape<K, R>;
   using T = typename std::conditional<VEC4, float4, float>::type;
   static constexpr int PER_ROW = VEC4 ? S::IW4 : S::IW4 * 4;
+  static constexpr int LDS_ROW = VEC4 ? S::LW4 : S::LW4 * 4;
   static constexpr int N = S::IH * PER_ROW;
   static constexpr int NL = (N + kBlock - 1) / kBlock;
   T v[NL];
@@ -112,7 +114,14 @@ struct Stager {
 #pragma unroll
     for (int j = 0; j < NL; ++j) {
       const int idx = threadIdx.x + j * kBlock;
-      if (NL * kBlock == N || idx < N) dst[idx] = v[j];
+      if (NL * kBlock == N || idx < N) {
+        if constexpr (LDS_ROW == PER_ROW) {
+          dst[idx] = v[j];
+        } else {
+          const int iy = idx / PER_ROW;
+          dst[iy * LDS_ROW + (idx - iy * PER_ROW)] = v[j];
+        }
+      }
     }
   }
 };
@@ -243,7 +252,7 @@ __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_ti
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
   const float4 *rowp = tile + wave * R * S::IW4 + lane;
 
-  Stager<K, R, VEC4> st;
+  Stager<S, VEC4> st;
   st.fetch(I, Wx, Wy, (wg / tiles_x) * S::TH, (wg % tiles_x) * kTileW);
   st.commit(tile);
   lds_barrier();
@@ -263,6 +272,178 @@ __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_ti
                          Hout, Wout, ostore);
     }
     if (m_end - m_begin > 1) load_filter<K>(F, m_begin, f);
+
+    lds_barrier();  // every wave is done reading this tile
+    if (more) st.commit(tile);
+    lds_barrier();  // the next tile is in LDS
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Matrix-core variant: banded filter rows on v_mfma_f32_4x4x1f32
+// ---------------------------------------------------------------------------
+// The instruction runs 16 independent 4x4 outer products per wave: lane
+// 4b + i supplies A[b][i], lane 4b + j supplies B[b][j], and lane 4b + j
+// receives D[b][i][j] in its register i.  Block b is a 4 x 4 output patch:
+// D[b][i][j] = O[y_b + j][x_b + i].  For filter row r, step t adds
+// A[i] * B[j] with A[i] = F[r][t - i] (zero outside 0..K-1) and
+// B[j] = I[y_b + j + r][x_b + t]; the K + 3 steps t = 0..K+2 of a row add
+// each of its K taps to all 16 outputs, so K of every K + 3 products are
+// useful (79% at K = 11).  A is the same for every block: a banded copy of
+// the filter, K x (K + 3) values per lane, held in accumulation registers
+// (the instruction reads its A operand from them directly).
+//
+// Sixteen blocks side by side make a 4-row x 64-column patch, and a wave
+// owns a column of P = 8 patches (32 rows x 64 columns).  It streams the
+// input rows of that column through registers once: lane 4b + j holds
+// input row u + j (four steps t at a time, one 16-byte LDS read), which is
+// row j + r of patch p for r = u - 4p, so one read feeds every patch with
+// 0 <= u - 4p < K (about K / 4 independent accumulation chains at once).
+
+template <int K>
+struct MfmaTileShape {
+  static constexpr int TH = 32;                 // output rows per tile: 8 per wave
+  static constexpr int IH = TH + K - 1;
+  static constexpr int NT = K + 3;              // steps per filter row
+  static constexpr int NQ = (NT + 3) / 4;       // 16-byte reads per patch per filter row
+  static constexpr int IW4 = kLanes + NQ - 1;   // float4 staged per row (256 + K - 1 floats used)
+  // Row stride = 2 (mod 8) float4: the 8 lanes (2 blocks x 4 rows) of one
+  // 128-byte LDS access then touch 8 different 16-byte bank groups.
+  static constexpr int LW4 = IW4 + (10 - IW4 % 8) % 8;
+  static constexpr int LDS = IH * LW4 * 16 + 4 * K * NT * 4;
+};
+
+// Workgroups per compute unit: from K = 9 the band (108 to 154 registers)
+// and the eight patch accumulators leave room for one.
+template <int K> struct MfmaOcc { static constexpr int value = K >= 9 ? 1 : 2; };
+
+typedef float mf4 __attribute__((ext_vector_type(4)));
+
+// The A operands of filter m: every thread stages its share of the banded
+// table band[i][r][t] = F[m][r][t - i] in LDS, then each lane copies row
+// i = lane % 4 into accumulation registers.  Two barriers; the caller must
+// not be reading `band` (a K x (K + 3) x 4 float LDS array).
+template <int K>
+__device__ __forceinline__ void load_band(const float *__restrict__ F, int m, int lane,
+                                          float *band, float (&a)[K][K + 3]) {
+  constexpr int NT = K + 3;
+  const float *Fm = F + (size_t)m * K * K;
+  for (int idx = threadIdx.x; idx < 4 * K * NT; idx += kBlock) {
+    const int t = idx % NT;
+    const int r = (idx / NT) % K;
+    const int s = t - idx / (K * NT);
+    band[idx] = (s >= 0 && s < K) ? Fm[r * K + s] : 0.f;
+  }
+  __syncthreads();
+  const float *row = band + (lane & 3) * K * NT;
+#pragma unroll
+  for (int r = 0; r < K; ++r)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) a[r][t] = row[r * NT + t];
+#pragma unroll
+  for (int r = 0; r < K; ++r)
+#pragma unroll
+    for (int t = 0; t < NT; ++t) asm volatile("" : "+a"(a[r][t]));
+  __syncthreads();
+}
+
+template <int K>
+__global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
+    const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
+    int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int ostore) {
+  using S = MfmaTileShape<K>;
+  constexpr int NT = S::NT, NQ = S::NQ, LW4 = S::LW4;
+  __shared__ float4 tile[S::IH * LW4];
+  __shared__ float band[4 * K * NT];
+
+  const int Hout = Wy - K + 1;
+  const int Wout = Wx - K + 1;
+  const int nwg = gridDim.x;
+  const int wg = xcd_remap(blockIdx.x, nwg);
+  if (wg >= ntiles) return;
+  const int m_begin = blockIdx.y * m_per_block;
+  const int m_end = min(M, m_begin + m_per_block);
+
+  const int lane = threadIdx.x & (kLanes - 1);
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
+  const int blk = lane >> 2;   // block: output columns 4 * blk .. +3 of a patch
+  const int q4 = lane & 3;     // output row of the lane (B, D roles)
+
+  Stager<S, true> st;
+  st.fetch(I, Wx, Wy, (wg / tiles_x) * S::TH, (wg % tiles_x) * kTileW);
+  st.commit(tile);
+  lds_barrier();
+
+  float a[K][NT];
+  load_band<K>(F, m_begin, lane, band, a);
+  for (int t = wg; t < ntiles; t += nwg) {
+    const int y0 = (t / tiles_x) * S::TH;
+    const int x0 = (t % tiles_x) * kTileW;
+    const int tn = t + nwg;
+    const bool more = tn < ntiles;
+    if (more) st.fetch(I, Wx, Wy, (tn / tiles_x) * S::TH, (tn % tiles_x) * kTileW);
+
+    for (int m = m_begin; m < m_end; ++m) {
+      if (m != m_begin) load_band<K>(F, m, lane, band, a);
+      float *Om = O + (size_t)m * Hout * Wout;
+      // Input rows u = 0 .. 4P + K - 5 of this wave's column (row u + j in
+      // lane 4b + j); output patch p (rows 4p .. 4p + 3) takes row u with
+      // filter row u - 4p.
+      constexpr int P = 8, U = 4 * P + K - 4;
+      const float4 *src = tile + q4 * LW4 + wave * 16 + blk;
+      mf4 acc[P];
+#pragma unroll
+      for (int p = 0; p < P; ++p) acc[p] = (mf4){0.f, 0.f, 0.f, 0.f};
+      float4 cb[NQ], nb[NQ];
+#pragma unroll
+      for (int q = 0; q < NQ; ++q) cb[q] = src[q];
+#pragma unroll
+      for (int u = 0; u < U; ++u) {
+        if (u + 1 < U) {
+#pragma unroll
+          for (int q = 0; q < NQ; ++q) nb[q] = src[(u + 1) * LW4 + q];
+        }
+#pragma unroll
+        for (int q = 0; q < NQ; ++q)
+#pragma unroll
+          for (int e = 0; e < 4; ++e) {
+            if (4 * q + e >= NT) continue;
+            const float bv = e == 0 ? cb[q].x : e == 1 ? cb[q].y : e == 2 ? cb[q].z : cb[q].w;
+#pragma unroll
+            for (int p = 0; p < P; ++p) {
+              const int r = u - 4 * p;
+              if (r >= 0 && r < K)
+                acc[p] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[r][4 * q + e], bv, acc[p], 0, 0, 0);
+            }
+          }
+#pragma unroll
+        for (int p = 0; p < P; ++p) asm volatile("" : "+a"(acc[p]));
+        __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+        for (int q = 0; q < NQ; ++q) cb[q] = nb[q];
+      }
+      // Lane holds output row y0 + 4p + q4, columns x0 + 4 * (16 wave + blk) + 0..3.
+      const int gx = x0 + 4 * (wave * 16 + blk);
+#pragma unroll
+      for (int p = 0; p < P; ++p) {
+        const int gy = y0 + 4 * p + q4;
+        if (gy >= Hout) continue;
+        float *orow = Om + (size_t)gy * Wout + gx;
+        const mf4 v = acc[p];
+        if (gx + 4 <= Wout && ostore == 4) {
+          __builtin_nontemporal_store((vf4){v[0], v[1], v[2], v[3]},
+                                      reinterpret_cast<vf4 *>(orow));
+        } else if (gx + 4 <= Wout && ostore == 2) {
+          __builtin_nontemporal_store((vf2){v[0], v[1]}, reinterpret_cast<vf2 *>(orow));
+          __builtin_nontemporal_store((vf2){v[2], v[3]}, reinterpret_cast<vf2 *>(orow) + 1);
+        } else {
+#pragma unroll
+          for (int w = 0; w < 4; ++w)
+            if (gx + w < Wout) __builtin_nontemporal_store(v[w], orow + w);
+        }
+      }
+    }
+    if (m_end - m_begin > 1) load_band<K>(F, m_begin, lane, band, a);
 
     lds_barrier();  // every wave is done reading this tile
     if (more) st.commit(tile);
@@ -294,22 +475,18 @@ __global__ __launch_bounds__(256) void single_generic(
   O[idx] = acc;
 }
 
-template <int K, bool VEC4>
-void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
-  constexpr int R = Rows<K, VEC4>::value;
-  using S = TileShape<K, R>;
+// Persistent workgroups: as many as fit on the chip at once.  Filters reuse
+// the staged tile; they are split over workgroups only as far as needed to
+// fill the chip when there are fewer tiles than slots.
+void plan_persistent(int Wx, int Wy, int K, int M, int num_cu, int th, int occupancy,
+                     SinglePlan *p) {
   const int Hout = Wy - K + 1, Wout = Wx - K + 1;
-  p->kernel = VEC4 ? 0 : 2;
-  p->rows = R;
-  p->tile_h = S::TH;
+  p->tile_h = th;
   p->tile_w = kTileW;
   p->tiles_x = (Wout + kTileW - 1) / kTileW;
-  p->tiles_y = (Hout + S::TH - 1) / S::TH;
+  p->tiles_y = (Hout + th - 1) / th;
   const int ntiles = p->tiles_x * p->tiles_y;
-  // Persistent workgroups: as many as fit on the chip at once.  Filters
-  // reuse the staged tile; they are split over workgroups only as far as
-  // needed to fill the chip when there are fewer tiles than slots.
-  const int slots = Occupancy<K, VEC4>::value * num_cu;
+  const int slots = occupancy * num_cu;
   int splits = (slots + ntiles - 1) / ntiles;
   if (splits > M) splits = M;
   if (splits < 1) splits = 1;
@@ -319,6 +496,27 @@ void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
   if (per_split < 1) per_split = 1;
   p->grid = ntiles < per_split ? ntiles : per_split;
   p->block = kBlock;
+}
+
+template <int K, bool VEC4>
+void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
+  constexpr int R = Rows<K, VEC4>::value;
+  using S = TileShape<K, R>;
+  p->kernel = VEC4 ? 0 : 2;
+  p->rows = R;
+  plan_persistent(Wx, Wy, K, M, num_cu, S::TH, Occupancy<K, VEC4>::value, p);
+  p->lds_bytes = S::LDS;
+}
+
+// Matrix-core kernels exist for K = kMfmaMinK .. kMaxTiledK.
+constexpr int kMfmaMinK = 5;
+
+template <int K>
+void plan_mfma(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
+  using S = MfmaTileShape<K>;
+  p->kernel = 3;
+  p->rows = 8;
+  plan_persistent(Wx, Wy, K, M, num_cu, S::TH, MfmaOcc<K>::value, p);
   p->lds_bytes = S::LDS;
 }
 
@@ -337,6 +535,13 @@ hipError_t launch_tiled(const SinglePlan &p, const float *I, const float *F, flo
                         int Wx, int Wy, int M, hipStream_t s) {
   const int ostore = store_width(O, Wx - K + 1);
   const int ntiles = p.tiles_x * p.tiles_y;
+  if constexpr (K >= kMfmaMinK) {
+    if (p.kernel == 3) {
+      hipLaunchKernelGGL(single_mfma<K>, dim3(p.grid, p.grid_z), dim3(kBlock), 0, s, I, F, O, Wx,
+                         Wy, M, p.tiles_x, ntiles, p.m_per_block, ostore);
+      return hipGetLastError();
+    }
+  }
   if (p.kernel == 0)
     hipLaunchKernelGGL((single_tiled<K, Rows<K, true>::value, true>), dim3(p.grid, p.grid_z),
                        dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block,
@@ -350,17 +555,26 @@ hipError_t launch_tiled(const SinglePlan &p, const float *I, const float *F, flo
 
 }  // namespace
 
-void plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, SinglePlan *p) {
+int plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, int variant,
+                SinglePlan *p) {
   *p = SinglePlan{};
   p->K = K;
   // 16-byte aligned rows: whole float4 staging loads.
   const bool vec4 = aligned && (Wx % 4 == 0);
+  // The matrix-core kernel needs float4 staging.  It runs only when forced:
+  // measured on a 4096 x 4096 map it ties the vector kernel at K = 7 and
+  // trails it at K = 9 (52 vs 44 us) and K = 11 (67 vs 58 us), so the
+  // automatic choice is the vector kernel.
+  const bool can_mfma = vec4 && K >= kMfmaMinK && K <= kMaxTiledK;
+  if (variant == DCONV_VARIANT_MFMA && !can_mfma) return DCONV_EUNSUPPORTED;
+  const bool mfma = variant == DCONV_VARIANT_MFMA;
   switch (K) {
 #define DCONV_PLAN_K(k)                                              \
   case k:                                                            \
-    if (vec4) plan_tiled<k, true>(Wx, Wy, M, num_cu, p);             \
+    if (mfma) plan_mfma<(k >= kMfmaMinK ? k : kMfmaMinK)>(Wx, Wy, M, num_cu, p); \
+    else if (vec4) plan_tiled<k, true>(Wx, Wy, M, num_cu, p);        \
     else plan_tiled<k, false>(Wx, Wy, M, num_cu, p);                 \
-    return;
+    return DCONV_OK;
     DCONV_PLAN_K(1) DCONV_PLAN_K(2) DCONV_PLAN_K(3) DCONV_PLAN_K(4) DCONV_PLAN_K(5)
     DCONV_PLAN_K(6) DCONV_PLAN_K(7) DCONV_PLAN_K(8) DCONV_PLAN_K(9) DCONV_PLAN_K(10)
     DCONV_PLAN_K(11)
@@ -380,6 +594,7 @@ void plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, SingleP
   p->m_per_block = M;
   p->block = 256;
   p->lds_bytes = 0;
+  return DCONV_OK;
 }
 
 hipError_t launch_single(const SinglePlan &p, const float *I, const float *F, float *O,

@@ -32,8 +32,8 @@ VARIANT_VALU = 1
 VARIANT_MFMA = 2
 _VARIANTS = {"auto": VARIANT_AUTO, "valu": VARIANT_VALU, "mfma": VARIANT_MFMA}
 
-EXPORTED = ("dconv_single", "dconv_multi", "dconv_multi_variant", "dconv_strerror",
-            "dconv_plan_single", "dconv_plan_multi", "dconv_plan_multi_candidates",
+EXPORTED = ("dconv_single", "dconv_single_variant", "dconv_multi", "dconv_multi_variant",
+            "dconv_strerror", "dconv_plan_single", "dconv_plan_single_variant", "dconv_plan_multi", "dconv_plan_multi_candidates",
             "dconv_multi_with_plan", "dconv_model_latency", "dconv_model_single",
             "dconv_model_multi", "dconv_plan_multi_paper", "dconv_probe_latency")
 
@@ -123,6 +123,10 @@ def load(path: str | None = None):
     vp, i = ctypes.c_void_p, ctypes.c_int
     lib.dconv_single.argtypes = [vp, vp, vp, i, i, i, i, vp]
     lib.dconv_single.restype = i
+    lib.dconv_single_variant.argtypes = [vp, vp, vp, i, i, i, i, i, vp]
+    lib.dconv_single_variant.restype = i
+    lib.dconv_plan_single_variant.argtypes = [i, i, i, i, i, i, ctypes.POINTER(Plan)]
+    lib.dconv_plan_single_variant.restype = i
     lib.dconv_multi.argtypes = [vp, vp, vp, i, i, i, i, i, vp]
     lib.dconv_multi.restype = i
     lib.dconv_multi_variant.argtypes = [vp, vp, vp, i, i, i, i, i, i, vp]
@@ -199,8 +203,12 @@ class _OnDevice:
             torch.cuda.set_device(self.prev)
 
 
-def single(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None) -> torch.Tensor:
-    """Eq. 2: ``I[Wy, Wx]``, ``F[M, K, K]`` -> ``O[M, Wy-K+1, Wx-K+1]`` (fp32)."""
+def single(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None,
+           variant: str = "auto") -> torch.Tensor:
+    """Eq. 2: ``I[Wy, Wx]``, ``F[M, K, K]`` -> ``O[M, Wy-K+1, Wx-K+1]`` (fp32).
+
+    ``variant`` forces the kernel family: ``"auto"``, ``"valu"`` or ``"mfma"``.
+    """
     _require(I, "I", 2)
     _require(F, "F", 3)
     Wy, Wx = I.shape
@@ -211,6 +219,8 @@ def single(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None) ->
         raise ValueError("I and F must be on the same device")
     if not (1 <= K <= min(Wx, Wy)):
         raise ValueError("need 1 <= K <= min(Wx, Wy)")
+    if variant not in _VARIANTS:
+        raise ValueError("variant must be one of %s" % sorted(_VARIANTS))
     shape = (M, Wy - K + 1, Wx - K + 1)
     if out is None:
         out = torch.empty(shape, dtype=torch.float32, device=I.device)
@@ -219,8 +229,8 @@ def single(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None) ->
         if tuple(out.shape) != shape or out.device != I.device:
             raise ValueError("out must be %r on %s" % (shape, I.device))
     with _OnDevice(I.device):
-        rc = load().dconv_single(I.data_ptr(), F.data_ptr(), out.data_ptr(), Wx, Wy, K, M,
-                                 _stream(I.device))
+        rc = load().dconv_single_variant(I.data_ptr(), F.data_ptr(), out.data_ptr(), Wx, Wy, K,
+                                         M, _VARIANTS[variant], _stream(I.device))
     _check(rc)
     return out
 
@@ -264,10 +274,12 @@ def multi(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None,
     return out
 
 
-def plan_single(Wx: int, Wy: int, K: int, M: int, num_cu: int = 256) -> dict:
-    """The launch plan ``dconv_single`` would use (host logic, no device)."""
+def plan_single(Wx: int, Wy: int, K: int, M: int, num_cu: int = 256,
+                variant: str = "auto") -> dict:
+    """The launch plan ``dconv_single_variant`` would use (host logic, no device)."""
     p = Plan()
-    _check(load().dconv_plan_single(Wx, Wy, K, M, num_cu, ctypes.byref(p)))
+    _check(load().dconv_plan_single_variant(Wx, Wy, K, M, _VARIANTS[variant], num_cu,
+                                            ctypes.byref(p)))
     return p.as_dict()
 
 

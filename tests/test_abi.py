@@ -93,16 +93,17 @@ def test_strerror():
     assert dc.strerror(12345) == "unknown status"
 
 
-def _check_single_plan(Wx, Wy, K, M):
-    p = dc.plan_single(Wx, Wy, K, M)
+def _check_single_plan(Wx, Wy, K, M, variant="auto"):
+    p = dc.plan_single(Wx, Wy, K, M, variant=variant)
     Hout, Wout = Wy - K + 1, Wx - K + 1
     assert p["lds_bytes"] <= LDS_MAX
     assert p["block"] in (64, 128, 256, 512, 1024)
-    if p["kernel"] in (0, 2):   # persistent tiled kernel: each workgroup walks a run of tiles
+    if p["kernel"] in (0, 2, 3):   # persistent tiled kernels: each workgroup walks a run of tiles
         tiles_x = -(-Wout // p["tile_w"])
         tiles_y = -(-Hout // p["tile_h"])
         assert 1 <= p["grid_x"] <= tiles_x * tiles_y
         assert p["grid_x"] * p["grid_y"] <= 4 * 256
+        assert (p["kernel"] == 3) == (p["variant"] == dc.dconv.VARIANT_MFMA)
         assert p["grid_y"] * p["tile_m"] >= M
         assert (p["grid_y"] - 1) * p["tile_m"] < M
     else:
@@ -136,9 +137,10 @@ def test_plans_for_workloads(name):
     w = WORKLOADS[name]
     if w.kind == "single":
         p = _check_single_plan(w.Wx, w.Wy, w.K, w.M)
-        # enough workgroups to occupy 256 compute units at the large size
+        # persistent workgroups on every one of the 256 compute units at the
+        # large size
         if w.Wx >= 1024:
-            assert p["grid_x"] * p["grid_y"] >= 2 * 256
+            assert p["grid_x"] * p["grid_y"] >= 256
     else:
         for v in ("auto", "valu", "mfma"):
             _check_multi_plan(w.C, w.M, w.Wx, w.Wy, w.K, v)
@@ -151,6 +153,22 @@ def test_plans_for_workloads(name):
     (4096, 4096, 11, 1), (28, 28, 5, 512), (1024, 1024, 3, 32), (37, 1000, 9, 4)])
 def test_single_plan_shapes(shape):
     _check_single_plan(*shape)
+    _check_single_plan(*shape, variant="valu")
+    Wx, Wy, K, M = shape
+    if 5 <= K <= 11 and Wx % 4 == 0:
+        assert _check_single_plan(*shape, variant="mfma")["kernel"] == 3
+    else:
+        with pytest.raises(RuntimeError):
+            dc.plan_single(*shape, variant="mfma")
+
+
+def test_single_auto_uses_the_vector_kernel():
+    """The matrix-core single-map kernel runs only when forced (it measured
+    slower than the vector kernel for every K on a 4096 x 4096 map)."""
+    for K in range(1, 12):
+        assert dc.plan_single(4096, 4096, K, 1)["kernel"] == 0, K
+        if K >= 5:
+            assert dc.plan_single(4096, 4096, K, 1, variant="mfma")["kernel"] == 3
 
 
 @pytest.mark.parametrize("shape", [

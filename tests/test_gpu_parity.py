@@ -21,16 +21,24 @@ SINGLE = sorted(n for n, w in WORKLOADS.items() if w.kind == "single")
 MULTI = sorted(n for n, w in WORKLOADS.items() if w.kind == "multi")
 
 
+def single_families(Wx, K):
+    """Kernel families dconv_single can run for this shape (the matrix-core
+    family needs K in 5..11 and rows of a multiple of 4 floats)."""
+    return ["auto", "valu"] + (["mfma"] if 5 <= K <= 11 and Wx % 4 == 0 else [])
+
+
 @pytest.mark.parametrize("name", SINGLE)
 @pytest.mark.parametrize("variant", ["float", "int"])
 def test_single_workload(name, variant):
+    w = WORKLOADS[name]
     I, F = make(name, variant)
-    O = gpu_single(I, F)
     O64, A64 = oracle_single(I, F)
-    if variant == "int":
-        assert_exact(O, O64, name)
-    else:
-        assert_within(O, O64, A64, name)
+    for fam in single_families(w.Wx, w.K):
+        O = gpu_single(I, F, variant=fam)
+        if variant == "int":
+            assert_exact(O, O64, "%s/%s" % (name, fam))
+        else:
+            assert_within(O, O64, A64, "%s/%s" % (name, fam))
 
 
 @pytest.mark.parametrize("name", MULTI)
@@ -53,6 +61,9 @@ SINGLE_SHAPES = [
     (258, 70, 2, 4), (520, 65, 7, 2), (61, 200, 9, 1), (130, 45, 11, 3), (100, 80, 13, 2),
     (64, 64, 16, 1), (33, 40, 1, 5), (1030, 9, 4, 1), (96, 96, 6, 37), (80, 81, 8, 1),
     (90, 91, 10, 2),
+    # matrix-core kernel: tails of its 32 x 256 tiles and 4 x 64 patches, K = 5..11
+    (300, 70, 11, 2), (516, 41, 9, 1), (264, 100, 7, 3), (12, 12, 11, 1), (20, 37, 5, 4),
+    (68, 9, 8, 2), (1028, 35, 10, 1), (256, 256, 6, 1),
 ]
 
 
@@ -61,10 +72,13 @@ def test_single_shapes(shape):
     Wx, Wy, K, M = shape
     I, F = random_arrays(1, M, Wx, Wy, K, seed=sum(shape) * 7919)
     O64, A64 = oracle_single(I[0], F[:, 0])
-    assert_within(gpu_single(I[0], F[:, 0]), O64, A64, "single %r" % (shape,))
     Ii, Fi = random_arrays(1, M, Wx, Wy, K, seed=sum(shape) * 7919 + 1, variant="int")
     O64i, _ = oracle_single(Ii[0], Fi[:, 0])
-    assert_exact(gpu_single(Ii[0], Fi[:, 0]), O64i, "single int %r" % (shape,))
+    for fam in single_families(Wx, K):
+        assert_within(gpu_single(I[0], F[:, 0], variant=fam), O64, A64,
+                      "single %r %s" % (shape, fam))
+        assert_exact(gpu_single(Ii[0], Fi[:, 0], variant=fam), O64i,
+                     "single int %r %s" % (shape, fam))
 
 
 # (C, M, Wx, Wy, K): odd channel counts (the MFMA path pairs channels), M not a
