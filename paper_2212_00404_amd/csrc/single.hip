@@ -302,31 +302,41 @@ __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_ti
 
 template <int K>
 struct MfmaTileShape {
-  static constexpr int TH = 32;                 // output rows per tile: 8 per wave
+  static constexpr int P = 4;                   // patches (4 rows each) per wave column
+  static constexpr int TH = 4 * P;              // output rows per tile
   static constexpr int IH = TH + K - 1;
   static constexpr int NT = K + 3;              // steps per filter row
-  static constexpr int NQ = (NT + 3) / 4;       // 16-byte reads per patch per filter row
+  static constexpr int NQ = (NT + 3) / 4;       // 16-byte reads per input row
   static constexpr int IW4 = kLanes + NQ - 1;   // float4 staged per row (256 + K - 1 floats used)
   // Row stride = 2 (mod 8) float4: the 8 lanes (2 blocks x 4 rows) of one
   // 128-byte LDS access then touch 8 different 16-byte bank groups.
   static constexpr int LW4 = IW4 + (10 - IW4 % 8) % 8;
-  static constexpr int LDS = IH * LW4 * 16 + 4 * K * NT * 4;
+  static constexpr int BUF4 = IH * LW4;         // one tile buffer, float4
+  static constexpr int LDS = 2 * BUF4 * 16 + 4 * K * NT * 4;
 };
 
-// Workgroups per compute unit: from K = 9 the band (108 to 154 registers)
-// and the eight patch accumulators leave room for one.
-template <int K> struct MfmaOcc { static constexpr int value = K >= 9 ? 1 : 2; };
+// Two workgroups per compute unit (the two tile buffers and the band fit
+// twice in LDS; accumulators, band and input rows in 2 x 128 registers).
+template <int K> struct MfmaOcc { static constexpr int value = 2; };
 
 typedef float mf4 __attribute__((ext_vector_type(4)));
+typedef __attribute__((address_space(3))) void *lds_ptr;
+
+// Direct global->LDS copy of 16 bytes per lane: lane l's float4 from `src`
+// lands at dst + l (dst is wave-uniform).
+__device__ __forceinline__ void dma_f128(const float *src, float4 *dst) {
+  __builtin_amdgcn_global_load_lds(src, (lds_ptr)dst, 16, 0, 0);
+}
 
 // The A operands of filter m: every thread stages its share of the banded
 // table band[i][r][t] = F[m][r][t - i] in LDS, then each lane copies row
-// i = lane % 4 into accumulation registers.  Two barriers; the caller must
-// not be reading `band` (a K x (K + 3) x 4 float LDS array).
+// i = lane % 4 into registers.  Two barriers; the caller must not be
+// reading `band` (a K x (K + 3) x 4 float LDS array).
 template <int K>
 __device__ __forceinline__ void load_band(const float *__restrict__ F, int m, int lane,
                                           float *band, float (&a)[K][K + 3]) {
   constexpr int NT = K + 3;
+  constexpr int P = MfmaTileShape<K>::P;
   const float *Fm = F + (size_t)m * K * K;
   for (int idx = threadIdx.x; idx < 4 * K * NT; idx += kBlock) {
     const int t = idx % NT;
@@ -340,11 +350,40 @@ __device__ __forceinline__ void load_band(const float *__restrict__ F, int m, in
   for (int r = 0; r < K; ++r)
 #pragma unroll
     for (int t = 0; t < NT; ++t) a[r][t] = row[r * NT + t];
+  // The first KA rows go to accumulation registers, the rest to ordinary
+  // vector registers (the instruction takes A from either): with the patch
+  // accumulators that keeps each file within the 128 registers a wave has
+  // when two workgroups share a compute unit.
+  constexpr int KA = (128 - 8 * P) / NT < K ? (128 - 8 * P) / NT : K;
 #pragma unroll
   for (int r = 0; r < K; ++r)
 #pragma unroll
-    for (int t = 0; t < NT; ++t) asm volatile("" : "+a"(a[r][t]));
+    for (int t = 0; t < NT; ++t) {
+      if (r < KA)
+        asm volatile("" : "+a"(a[r][t]));
+      else
+        asm volatile("" : "+v"(a[r][t]));
+    }
   __syncthreads();
+}
+
+// Stage the tile at (y0, x0) into `buf` with direct global->LDS copies (no
+// registers): wave w copies rows w, w + 4, ...  Rows and columns past the
+// map re-read its last row / last float4; they feed only outputs that are
+// never stored.
+template <int K>
+__device__ __forceinline__ void stage_tile(const float *__restrict__ I, int Wx, int Wy, int y0,
+                                           int x0, float4 *buf, int wave, int lane) {
+  using S = MfmaTileShape<K>;
+  for (int row = wave; row < S::IH; row += kWaves) {
+    const float *srow = I + (size_t)min(y0 + row, Wy - 1) * Wx;
+#pragma unroll
+    for (int c = 0; c < S::IW4; c += kLanes) {
+      const int ix = c + lane;
+      if (c + kLanes <= S::IW4 || ix < S::IW4)
+        dma_f128(srow + min(x0 + 4 * ix, Wx - 4), buf + row * S::LW4 + c);
+    }
+  }
 }
 
 template <int K>
@@ -352,8 +391,8 @@ __global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
     const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
     int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int ostore) {
   using S = MfmaTileShape<K>;
-  constexpr int NT = S::NT, NQ = S::NQ, LW4 = S::LW4;
-  __shared__ float4 tile[S::IH * LW4];
+  constexpr int NT = S::NT, NQ = S::NQ, LW4 = S::LW4, P = S::P;
+  __shared__ float4 tiles[2 * S::BUF4];
   __shared__ float band[4 * K * NT];
 
   const int Hout = Wy - K + 1;
@@ -369,31 +408,40 @@ __global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
   const int blk = lane >> 2;   // block: output columns 4 * blk .. +3 of a patch
   const int q4 = lane & 3;     // output row of the lane (B, D roles)
 
-  Stager<S, true> st;
-  st.fetch(I, Wx, Wy, (wg / tiles_x) * S::TH, (wg % tiles_x) * kTileW);
-  st.commit(tile);
-  lds_barrier();
-
   float a[K][NT];
   load_band<K>(F, m_begin, lane, band, a);
+  stage_tile<K>(I, Wx, Wy, (wg / tiles_x) * S::TH, (wg % tiles_x) * kTileW, tiles, wave, lane);
+  int cur = 0;
   for (int t = wg; t < ntiles; t += nwg) {
     const int y0 = (t / tiles_x) * S::TH;
     const int x0 = (t % tiles_x) * kTileW;
+    // Tile t is in buffer `cur` once this wave's copies (and stores) have
+    // completed and every wave has passed the barrier; every wave is then
+    // also done with the other buffer, which takes the next tile's copies
+    // while this one is computed.
+    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    lds_barrier();
     const int tn = t + nwg;
-    const bool more = tn < ntiles;
-    if (more) st.fetch(I, Wx, Wy, (tn / tiles_x) * S::TH, (tn % tiles_x) * kTileW);
+    if (tn < ntiles)
+      stage_tile<K>(I, Wx, Wy, (tn / tiles_x) * S::TH, (tn % tiles_x) * kTileW,
+                    tiles + (cur ^ 1) * S::BUF4, wave, lane);
+    const float4 *tile = tiles + cur * S::BUF4;
+    cur ^= 1;
 
     for (int m = m_begin; m < m_end; ++m) {
       if (m != m_begin) load_band<K>(F, m, lane, band, a);
       float *Om = O + (size_t)m * Hout * Wout;
       // Input rows u = 0 .. 4P + K - 5 of this wave's column (row u + j in
       // lane 4b + j); output patch p (rows 4p .. 4p + 3) takes row u with
-      // filter row u - 4p.
-      constexpr int P = 8, U = 4 * P + K - 4;
+      // filter row u - 4p and is stored after its last row, u = 4p + K - 1.
+      constexpr int U = 4 * P + K - 4;
       const float4 *src = tile + q4 * LW4 + wave * 16 + blk;
-      mf4 acc[P];
+      const int gx = x0 + 4 * (wave * 16 + blk);
+      // Two accumulators per patch (even and odd steps t) keep at least two
+      // independent chains in flight where only one patch takes a row.
+      mf4 acc[P][2];
 #pragma unroll
-      for (int p = 0; p < P; ++p) acc[p] = (mf4){0.f, 0.f, 0.f, 0.f};
+      for (int p = 0; p < P; ++p) acc[p][0] = acc[p][1] = (mf4){0.f, 0.f, 0.f, 0.f};
       float4 cb[NQ], nb[NQ];
 #pragma unroll
       for (int q = 0; q < NQ; ++q) cb[q] = src[q];
@@ -413,41 +461,39 @@ __global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
             for (int p = 0; p < P; ++p) {
               const int r = u - 4 * p;
               if (r >= 0 && r < K)
-                acc[p] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[r][4 * q + e], bv, acc[p], 0, 0, 0);
+                acc[p][e & 1] = __builtin_amdgcn_mfma_f32_4x4x1f32(a[r][4 * q + e], bv,
+                                                                   acc[p][e & 1], 0, 0, 0);
             }
           }
 #pragma unroll
-        for (int p = 0; p < P; ++p) asm volatile("" : "+a"(acc[p]));
+        for (int p = 0; p < P; ++p) {
+          if (u != 4 * p + K - 1) continue;
+          // Patch p is complete: this lane holds output row y0 + 4p + q4,
+          // columns gx .. gx + 3.
+          const int gy = y0 + 4 * p + q4;
+          if (gy >= Hout) continue;
+          float *orow = Om + (size_t)gy * Wout + gx;
+          const mf4 v = acc[p][0] + acc[p][1];
+          if (gx + 4 <= Wout && ostore == 4) {
+            __builtin_nontemporal_store((vf4){v[0], v[1], v[2], v[3]},
+                                        reinterpret_cast<vf4 *>(orow));
+          } else if (gx + 4 <= Wout && ostore == 2) {
+            __builtin_nontemporal_store((vf2){v[0], v[1]}, reinterpret_cast<vf2 *>(orow));
+            __builtin_nontemporal_store((vf2){v[2], v[3]}, reinterpret_cast<vf2 *>(orow) + 1);
+          } else {
+#pragma unroll
+            for (int w = 0; w < 4; ++w)
+              if (gx + w < Wout) __builtin_nontemporal_store(v[w], orow + w);
+          }
+        }
+#pragma unroll
+        for (int p = 0; p < P; ++p) asm volatile("" : "+a"(acc[p][0]), "+a"(acc[p][1]));
         __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
         for (int q = 0; q < NQ; ++q) cb[q] = nb[q];
       }
-      // Lane holds output row y0 + 4p + q4, columns x0 + 4 * (16 wave + blk) + 0..3.
-      const int gx = x0 + 4 * (wave * 16 + blk);
-#pragma unroll
-      for (int p = 0; p < P; ++p) {
-        const int gy = y0 + 4 * p + q4;
-        if (gy >= Hout) continue;
-        float *orow = Om + (size_t)gy * Wout + gx;
-        const mf4 v = acc[p];
-        if (gx + 4 <= Wout && ostore == 4) {
-          __builtin_nontemporal_store((vf4){v[0], v[1], v[2], v[3]},
-                                      reinterpret_cast<vf4 *>(orow));
-        } else if (gx + 4 <= Wout && ostore == 2) {
-          __builtin_nontemporal_store((vf2){v[0], v[1]}, reinterpret_cast<vf2 *>(orow));
-          __builtin_nontemporal_store((vf2){v[2], v[3]}, reinterpret_cast<vf2 *>(orow) + 1);
-        } else {
-#pragma unroll
-          for (int w = 0; w < 4; ++w)
-            if (gx + w < Wout) __builtin_nontemporal_store(v[w], orow + w);
-        }
-      }
     }
     if (m_end - m_begin > 1) load_band<K>(F, m_begin, lane, band, a);
-
-    lds_barrier();  // every wave is done reading this tile
-    if (more) st.commit(tile);
-    lds_barrier();  // the next tile is in LDS
   }
 }
 
