@@ -150,7 +150,8 @@ def test_plans_for_workloads(name):
 
 @pytest.mark.parametrize("shape", [
     (1, 1, 1, 1), (5, 7, 3, 2), (300, 17, 5, 3), (64, 64, 11, 1), (100, 80, 13, 2),
-    (4096, 4096, 11, 1), (28, 28, 5, 512), (1024, 1024, 3, 32), (37, 1000, 9, 4)])
+    (4096, 4096, 11, 1), (28, 28, 5, 512), (1024, 1024, 3, 32), (37, 1000, 9, 4),
+    (4100, 2100, 9, 1), (2052, 4000, 11, 2), (1024, 8192, 10, 1), (4096, 4096, 8, 100)])
 def test_single_plan_shapes(shape):
     _check_single_plan(*shape)
     _check_single_plan(*shape, variant="valu")

@@ -64,6 +64,9 @@ SINGLE_SHAPES = [
     # matrix-core kernel: tails of its 32 x 256 tiles and 4 x 64 patches, K = 5..11
     (300, 70, 11, 2), (516, 41, 9, 1), (264, 100, 7, 3), (12, 12, 11, 1), (20, 37, 5, 4),
     (68, 9, 8, 2), (1028, 35, 10, 1), (256, 256, 6, 1),
+    # large maps with K >= 8: ragged last tile column and row, unequal tile
+    # runs per persistent workgroup, two filters, an even K
+    (4100, 2100, 9, 1), (2052, 4000, 11, 2), (1024, 8192, 10, 1),
 ]
 
 
