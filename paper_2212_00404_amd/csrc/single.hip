@@ -69,6 +69,11 @@ struct TileShape {
   static constexpr int LDS = IH * LW4 * 16;
 };
 
+// s_waitcnt immediate for "vmcnt(0)" alone on gfx9-family chips: vmcnt in
+// bits 3:0 and 15:14 (0), expcnt in bits 6:4 and lgkmcnt in bits 11:8 at their
+// maxima (no wait).
+constexpr int kWaitVmcnt0 = 0x0F70;
+
 // Barrier for LDS hand-over inside a workgroup.  Unlike __syncthreads() it
 // does not wait for outstanding global loads (the next tile's prefetch stays
 // in flight across it) or global stores.
@@ -392,7 +397,9 @@ __global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
     int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int ostore) {
   using S = MfmaTileShape<K>;
   constexpr int NT = S::NT, NQ = S::NQ, LW4 = S::LW4, P = S::P;
-  __shared__ float4 tiles[2 * S::BUF4];
+  // Two tile buffers as separate LDS objects (see the loop below).
+  __shared__ float4 tile0[S::BUF4];
+  __shared__ float4 tile1[S::BUF4];
   __shared__ float band[4 * K * NT];
 
   const int Hout = Wy - K + 1;
@@ -410,23 +417,26 @@ __global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
 
   float a[K][NT];
   load_band<K>(F, m_begin, lane, band, a);
-  stage_tile<K>(I, Wx, Wy, (wg / tiles_x) * S::TH, (wg % tiles_x) * kTileW, tiles, wave, lane);
-  int cur = 0;
-  for (int t = wg; t < ntiles; t += nwg) {
+  stage_tile<K>(I, Wx, Wy, (wg / tiles_x) * S::TH, (wg % tiles_x) * kTileW, tile0, wave, lane);
+  // One tile: wait for its copies, start the next tile's copies into the
+  // other buffer, compute.  The wait is the compiler's own instruction (not
+  // inline assembly), so it knows every copy has landed; and since the two
+  // buffers are distinct LDS objects fixed at compile time in each call, it
+  // can tell that the copies just started cannot alias this tile's reads and
+  // adds no wait for them before the compute (with one array indexed at run
+  // time it waited for all copies in flight, serialising copy and compute).
+  auto step = [&](int t, const float4 *tile, float4 *next) {
     const int y0 = (t / tiles_x) * S::TH;
     const int x0 = (t % tiles_x) * kTileW;
-    // Tile t is in buffer `cur` once this wave's copies (and stores) have
+    // Tile t is in `tile` once this wave's copies (and stores) have
     // completed and every wave has passed the barrier; every wave is then
-    // also done with the other buffer, which takes the next tile's copies
-    // while this one is computed.
-    asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+    // also done with `next`, which takes the next tile's copies while this
+    // one is computed.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
     lds_barrier();
     const int tn = t + nwg;
     if (tn < ntiles)
-      stage_tile<K>(I, Wx, Wy, (tn / tiles_x) * S::TH, (tn % tiles_x) * kTileW,
-                    tiles + (cur ^ 1) * S::BUF4, wave, lane);
-    const float4 *tile = tiles + cur * S::BUF4;
-    cur ^= 1;
+      stage_tile<K>(I, Wx, Wy, (tn / tiles_x) * S::TH, (tn % tiles_x) * kTileW, next, wave, lane);
 
     for (int m = m_begin; m < m_end; ++m) {
       if (m != m_begin) load_band<K>(F, m, lane, band, a);
@@ -494,6 +504,11 @@ __global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
       }
     }
     if (m_end - m_begin > 1) load_band<K>(F, m_begin, lane, band, a);
+  };
+  for (int t = wg; t < ntiles; t += 2 * nwg) {
+    step(t, tile0, tile1);
+    if (t + nwg >= ntiles) break;
+    step(t + nwg, tile1, tile0);
   }
 }
 
