@@ -157,6 +157,12 @@ __device__ __forceinline__ void load_filter(const float *__restrict__ F, int m, 
     for (int r = 0; r < K; ++r)
 #pragma unroll
       for (int s = 0; s < K; ++s) f[r][s] = p[r * K + s];
+    // Wait for them here, with an instruction the compiler sees.  Otherwise
+    // the first use of the filter, at a point the load may or may not have
+    // been issued on every path, gets a wait for all loads in flight, which
+    // includes the next tile's prefetch: prefetch and compute would then not
+    // overlap even where no filter is reloaded.
+    __builtin_amdgcn_s_waitcnt(kWaitVmcnt0);
   } else {
 #pragma unroll
     for (int r = 0; r < K; ++r)
