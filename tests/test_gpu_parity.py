@@ -67,6 +67,9 @@ SINGLE_SHAPES = [
     # large maps with K >= 8: ragged last tile column and row, unequal tile
     # runs per persistent workgroup, two filters, an even K
     (4100, 2100, 9, 1), (2052, 4000, 11, 2), (1024, 8192, 10, 1),
+    # persistent workgroups with two or three tiles each (the matrix-core
+    # kernel walks tiles in pairs; an odd count ends on a single tile)
+    (4096, 1300, 7, 1), (4096, 1300, 11, 1),
 ]
 
 
