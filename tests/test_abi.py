@@ -9,6 +9,7 @@ import pytest
 
 import paper_2212_00404_amd as dc
 from dconv_workloads import WORKLOADS
+from random_shapes import MULTI_RANDOM, SINGLE_RANDOM
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
 HEADER = os.path.join(ROOT, "include", "dconv.h")
@@ -192,3 +193,16 @@ def test_small_maps_split_the_channel_sum():
     p = dc.plan_multi(512, 512, 9, 9, 3)
     assert p["split_c"] > 1
     assert p["grid_x"] >= 256
+
+
+@pytest.mark.parametrize("shape", SINGLE_RANDOM, ids=[str(s) for s in SINGLE_RANDOM])
+def test_single_plan_random(shape):
+    for v in ("auto", "valu"):
+        _check_single_plan(*shape, variant=v)
+
+
+@pytest.mark.parametrize("shape", MULTI_RANDOM, ids=[str(s) for s in MULTI_RANDOM])
+def test_multi_plan_random(shape):
+    for v in ("auto", "valu") + (("mfma",) if shape[4] <= 7 else ()):
+        _check_multi_plan(*shape, variant=v)
+
