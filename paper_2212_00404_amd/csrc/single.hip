@@ -34,8 +34,14 @@ constexpr int kWaves = 4;
 constexpr int kBlock = kLanes * kWaves;
 constexpr int kTileW = kLanes * kW;  // 256 output columns per tile
 
-typedef float vf4 __attribute__((ext_vector_type(4)));
-typedef float vf2 __attribute__((ext_vector_type(2)));
+// A lane's 4 output columns, stored as one 16-byte write.  Rows of O start
+// wherever Wout puts them, so the type asks for 4-byte alignment only: the
+// chip's global stores need dword alignment, and one 16-byte store per lane
+// keeps every write a whole run of the row.  (Two 8-byte or four 4-byte
+// non-temporal stores per lane, as an odd or 2 (mod 4) width would otherwise
+// need, leave partly written lines: measured 1.05x slower at Wout = 4090 and
+// 1.8-2.6x slower at Wout = 4089 and 4091.)
+typedef float vf4u __attribute__((ext_vector_type(4), aligned(4)));
 
 // Output rows per lane: enough that halo re-reads stay small, few enough that
 // accumulators, filter, input rows and the prefetched tile fit in VGPRs (a
@@ -175,7 +181,7 @@ __device__ __forceinline__ void load_filter(const float *__restrict__ F, int m, 
 template <int K, int R>
 __device__ __forceinline__ void apply_filter(const float4 *rowp, const float (&f)[K][K],
                                              float *__restrict__ Om, int oy0, int ox0, int Hout,
-                                             int Wout, int ostore) {
+                                             int Wout) {
   using S = TileShape<K, R>;
   constexpr int IW4 = S::IW4, NQ = S::NQ;
   constexpr int G = Group<K>::value;
@@ -226,12 +232,9 @@ __device__ __forceinline__ void apply_filter(const float4 *rowp, const float (&f
       // non-temporal stores keep it from displacing the input tiles and
       // halos in the caches (measured: 15-20% faster across K).
       float *orow = Om + (size_t)y * Wout + ox0;
-      if (ox0 + kW <= Wout && ostore == 4) {
-        __builtin_nontemporal_store((vf4){acc[j][0], acc[j][1], acc[j][2], acc[j][3]},
-                                    reinterpret_cast<vf4 *>(orow));
-      } else if (ox0 + kW <= Wout && ostore == 2) {
-        __builtin_nontemporal_store((vf2){acc[j][0], acc[j][1]}, reinterpret_cast<vf2 *>(orow));
-        __builtin_nontemporal_store((vf2){acc[j][2], acc[j][3]}, reinterpret_cast<vf2 *>(orow) + 1);
+      if (ox0 + kW <= Wout) {
+        __builtin_nontemporal_store((vf4u){acc[j][0], acc[j][1], acc[j][2], acc[j][3]},
+                                    reinterpret_cast<vf4u *>(orow));
       } else {
 #pragma unroll
         for (int w = 0; w < kW; ++w)
@@ -244,7 +247,7 @@ __device__ __forceinline__ void apply_filter(const float4 *rowp, const float (&f
 template <int K, int R, bool VEC4>
 __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_tiled(
     const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
-    int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int ostore) {
+    int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block) {
   using S = TileShape<K, R>;
   __shared__ float4 tile[S::IH * S::IW4];
 
@@ -280,7 +283,7 @@ __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_ti
     for (int m = m_begin; m < m_end; ++m) {
       if (m != m_begin) load_filter<K>(F, m, f);
       apply_filter<K, R>(rowp, f, O + (size_t)m * Hout * Wout, y0 + wave * R, x0 + lane * kW,
-                         Hout, Wout, ostore);
+                         Hout, Wout);
     }
     if (m_end - m_begin > 1) load_filter<K>(F, m_begin, f);
 
@@ -400,7 +403,7 @@ __device__ __forceinline__ void stage_tile(const float *__restrict__ I, int Wx, 
 template <int K>
 __global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
     const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
-    int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block, int ostore) {
+    int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block) {
   using S = MfmaTileShape<K>;
   constexpr int NT = S::NT, NQ = S::NQ, LW4 = S::LW4, P = S::P;
   // Two tile buffers as separate LDS objects (see the loop below).
@@ -490,12 +493,9 @@ __global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
           if (gy >= Hout) continue;
           float *orow = Om + (size_t)gy * Wout + gx;
           const mf4 v = acc[p][0] + acc[p][1];
-          if (gx + 4 <= Wout && ostore == 4) {
-            __builtin_nontemporal_store((vf4){v[0], v[1], v[2], v[3]},
-                                        reinterpret_cast<vf4 *>(orow));
-          } else if (gx + 4 <= Wout && ostore == 2) {
-            __builtin_nontemporal_store((vf2){v[0], v[1]}, reinterpret_cast<vf2 *>(orow));
-            __builtin_nontemporal_store((vf2){v[2], v[3]}, reinterpret_cast<vf2 *>(orow) + 1);
+          if (gx + 4 <= Wout) {
+            __builtin_nontemporal_store((vf4u){v[0], v[1], v[2], v[3]},
+                                        reinterpret_cast<vf4u *>(orow));
           } else {
 #pragma unroll
             for (int w = 0; w < 4; ++w)
@@ -587,36 +587,23 @@ void plan_mfma(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
   p->lds_bytes = S::LDS;
 }
 
-// Widest output store every row of O allows: 4 floats if rows start on 16-byte
-// boundaries, 2 if on 8-byte boundaries, else 1.  Lanes own 4 columns at
-// multiples of 4, so aligned rows keep every lane's store aligned.
-int store_width(const float *O, int Wout) {
-  const uintptr_t a = reinterpret_cast<uintptr_t>(O);
-  if (Wout % 4 == 0 && (a & 15) == 0) return 4;
-  if (Wout % 2 == 0 && (a & 7) == 0) return 2;
-  return 1;
-}
-
 template <int K>
 hipError_t launch_tiled(const SinglePlan &p, const float *I, const float *F, float *O,
                         int Wx, int Wy, int M, hipStream_t s) {
-  const int ostore = store_width(O, Wx - K + 1);
   const int ntiles = p.tiles_x * p.tiles_y;
   if constexpr (K >= kMfmaMinK) {
     if (p.kernel == 3) {
       hipLaunchKernelGGL(single_mfma<K>, dim3(p.grid, p.grid_z), dim3(kBlock), 0, s, I, F, O, Wx,
-                         Wy, M, p.tiles_x, ntiles, p.m_per_block, ostore);
+                         Wy, M, p.tiles_x, ntiles, p.m_per_block);
       return hipGetLastError();
     }
   }
   if (p.kernel == 0)
     hipLaunchKernelGGL((single_tiled<K, Rows<K, true>::value, true>), dim3(p.grid, p.grid_z),
-                       dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block,
-                       ostore);
+                       dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block);
   else
     hipLaunchKernelGGL((single_tiled<K, Rows<K, false>::value, false>), dim3(p.grid, p.grid_z),
-                       dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block,
-                       ostore);
+                       dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block);
   return hipGetLastError();
 }
 
