@@ -178,7 +178,8 @@ __device__ __forceinline__ void load_filter(const float *__restrict__ F, int m, 
 }
 
 // One filter over the staged tile: this lane's R x 4 outputs at (oy0, ox0).
-template <int K, int R>
+// NT: non-temporal output stores.
+template <int K, int R, bool NT>
 __device__ __forceinline__ void apply_filter(const float4 *rowp, const float (&f)[K][K],
                                              float *__restrict__ Om, int oy0, int ox0, int Hout,
                                              int Wout) {
@@ -230,21 +231,25 @@ __device__ __forceinline__ void apply_filter(const float4 *rowp, const float (&f
       if (y >= Hout) continue;
       // The output is written once and never read back by this kernel:
       // non-temporal stores keep it from displacing the input tiles and
-      // halos in the caches (measured: 15-20% faster across K).
+      // halos in the caches (measured: 15-20% faster across K).  The
+      // exception (NT false) is chosen by the host.
       float *orow = Om + (size_t)y * Wout + ox0;
+      const vf4u v = {acc[j][0], acc[j][1], acc[j][2], acc[j][3]};
       if (ox0 + kW <= Wout) {
-        __builtin_nontemporal_store((vf4u){acc[j][0], acc[j][1], acc[j][2], acc[j][3]},
-                                    reinterpret_cast<vf4u *>(orow));
+        if constexpr (NT)
+          __builtin_nontemporal_store(v, reinterpret_cast<vf4u *>(orow));
+        else
+          *reinterpret_cast<vf4u *>(orow) = v;
       } else {
 #pragma unroll
         for (int w = 0; w < kW; ++w)
-          if (ox0 + w < Wout) __builtin_nontemporal_store(acc[j][w], orow + w);
+          if (ox0 + w < Wout) orow[w] = v[w];
       }
     }
   }
 }
 
-template <int K, int R, bool VEC4>
+template <int K, int R, bool VEC4, bool NT>
 __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_tiled(
     const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
     int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block) {
@@ -282,8 +287,8 @@ __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_ti
 
     for (int m = m_begin; m < m_end; ++m) {
       if (m != m_begin) load_filter<K>(F, m, f);
-      apply_filter<K, R>(rowp, f, O + (size_t)m * Hout * Wout, y0 + wave * R, x0 + lane * kW,
-                         Hout, Wout);
+      apply_filter<K, R, NT>(rowp, f, O + (size_t)m * Hout * Wout, y0 + wave * R,
+                             x0 + lane * kW, Hout, Wout);
     }
     if (m_end - m_begin > 1) load_filter<K>(F, m_begin, f);
 
@@ -587,6 +592,43 @@ void plan_mfma(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
   p->lds_bytes = S::LDS;
 }
 
+// Non-temporal output stores, except where rows of O do not start on
+// 16-byte boundaries, each workgroup writes four or more filters per tile
+// and the output is larger than the L2s together: there ordinary stores,
+// which L2 merges into whole lines, measured faster (1024 x 1024 map, K = 3,
+// 32 filters: 31.6 vs 39.7 us; 2048 x 2048, 4 filters: 15.4 vs 19.1 us).
+// With one or two filters per workgroup or aligned rows the non-temporal
+// stores are as fast or faster (4096 x 4096, K = 3, M = 1: 22.3 vs 26.3 us),
+// and on small outputs (112 x 112, 128 filters) slightly faster.  The
+// ordinary-store kernels exist for K <= kTemporalMaxK (the filter sizes of
+// the many-filter layers).
+constexpr int kTemporalMaxK = 5;
+constexpr int64_t kTemporalMinBytes = 32ll << 20;
+bool use_nt_stores(const SinglePlan &p, const float *O, int Wx, int Wy, int M) {
+  const int Hout = Wy - p.K + 1, Wout = Wx - p.K + 1;
+  const bool aligned_rows = Wout % 4 == 0 && (reinterpret_cast<uintptr_t>(O) & 15) == 0;
+  const int64_t out_bytes = (int64_t)M * Hout * Wout * 4;
+  return aligned_rows || p.m_per_block < 4 || p.K > kTemporalMaxK ||
+         out_bytes < kTemporalMinBytes;
+}
+
+template <int K, bool VEC4>
+void launch_vector(const SinglePlan &p, const float *I, const float *F, float *O, int Wx, int Wy,
+                   int M, bool nt, hipStream_t s) {
+  constexpr int R = Rows<K, VEC4>::value;
+  const int ntiles = p.tiles_x * p.tiles_y;
+  if constexpr (K <= kTemporalMaxK) {
+    if (!nt) {
+      hipLaunchKernelGGL((single_tiled<K, R, VEC4, false>), dim3(p.grid, p.grid_z),
+                         dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles,
+                         p.m_per_block);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((single_tiled<K, R, VEC4, true>), dim3(p.grid, p.grid_z), dim3(kBlock), 0,
+                     s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block);
+}
+
 template <int K>
 hipError_t launch_tiled(const SinglePlan &p, const float *I, const float *F, float *O,
                         int Wx, int Wy, int M, hipStream_t s) {
@@ -598,12 +640,11 @@ hipError_t launch_tiled(const SinglePlan &p, const float *I, const float *F, flo
       return hipGetLastError();
     }
   }
+  const bool nt = use_nt_stores(p, O, Wx, Wy, M);
   if (p.kernel == 0)
-    hipLaunchKernelGGL((single_tiled<K, Rows<K, true>::value, true>), dim3(p.grid, p.grid_z),
-                       dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block);
+    launch_vector<K, true>(p, I, F, O, Wx, Wy, M, nt, s);
   else
-    hipLaunchKernelGGL((single_tiled<K, Rows<K, false>::value, false>), dim3(p.grid, p.grid_z),
-                       dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block);
+    launch_vector<K, false>(p, I, F, O, Wx, Wy, M, nt, s);
   return hipGetLastError();
 }
 

@@ -70,6 +70,9 @@ SINGLE_SHAPES = [
     # persistent workgroups with two or three tiles each (the matrix-core
     # kernel walks tiles in pairs; an odd count ends on a single tile)
     (4096, 1300, 7, 1), (4096, 1300, 11, 1),
+    # rows of O off 16-byte boundaries, four filters per workgroup, output
+    # above 32 MB: the vector kernel with ordinary (not non-temporal) stores
+    (1024, 1024, 3, 16), (1030, 1000, 5, 16),
 ]
 
 
