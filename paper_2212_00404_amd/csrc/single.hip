@@ -54,6 +54,9 @@ typedef float vf4u __attribute__((ext_vector_type(4), aligned(4)));
 template <int K, bool VEC4> struct Rows {
   static constexpr int value = (K <= 5 || (!VEC4 && K >= 8)) ? 4 : 8;
 };
+// Rows per lane of the short tiles used where tall ones would not give every
+// compute unit a tile.
+constexpr int kShortRows = 4;
 // Output rows accumulated at once (a divisor of Rows).
 template <int K> struct Group { static constexpr int value = 4; };
 // Workgroups per compute unit the kernel is compiled for (register budget; a
@@ -578,6 +581,17 @@ void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
   p->rows = R;
   plan_persistent(Wx, Wy, K, M, num_cu, S::TH, Occupancy<K, VEC4>::value, p);
   p->lds_bytes = S::LDS;
+  if constexpr (R > kShortRows) {
+    // Fewer tall tiles than compute units (a small map with few filters):
+    // short tiles, twice as many (1024 x 1024, K = 7, M = 1: 128 tall tiles
+    // left half the chip idle).
+    if ((int64_t)p->tiles_x * p->tiles_y * p->grid_z < num_cu) {
+      using SS = TileShape<K, kShortRows>;
+      p->rows = kShortRows;
+      plan_persistent(Wx, Wy, K, M, num_cu, SS::TH, Occupancy<K, VEC4>::value, p);
+      p->lds_bytes = SS::LDS;
+    }
+  }
 }
 
 // Matrix-core kernels exist for K = kMfmaMinK .. kMaxTiledK.
@@ -612,10 +626,9 @@ bool use_nt_stores(const SinglePlan &p, const float *O, int Wx, int Wy, int M) {
          out_bytes < kTemporalMinBytes;
 }
 
-template <int K, bool VEC4>
+template <int K, bool VEC4, int R>
 void launch_vector(const SinglePlan &p, const float *I, const float *F, float *O, int Wx, int Wy,
                    int M, bool nt, hipStream_t s) {
-  constexpr int R = Rows<K, VEC4>::value;
   const int ntiles = p.tiles_x * p.tiles_y;
   if constexpr (K <= kTemporalMaxK) {
     if (!nt) {
@@ -641,10 +654,18 @@ hipError_t launch_tiled(const SinglePlan &p, const float *I, const float *F, flo
     }
   }
   const bool nt = use_nt_stores(p, O, Wx, Wy, M);
-  if (p.kernel == 0)
-    launch_vector<K, true>(p, I, F, O, Wx, Wy, M, nt, s);
-  else
-    launch_vector<K, false>(p, I, F, O, Wx, Wy, M, nt, s);
+  constexpr int RA = Rows<K, true>::value, RU = Rows<K, false>::value;
+  if (p.kernel == 0) {
+    if (RA > kShortRows && p.rows == kShortRows)
+      launch_vector<K, true, kShortRows>(p, I, F, O, Wx, Wy, M, nt, s);
+    else
+      launch_vector<K, true, RA>(p, I, F, O, Wx, Wy, M, nt, s);
+  } else {
+    if (RU > kShortRows && p.rows == kShortRows)
+      launch_vector<K, false, kShortRows>(p, I, F, O, Wx, Wy, M, nt, s);
+    else
+      launch_vector<K, false, RU>(p, I, F, O, Wx, Wy, M, nt, s);
+  }
   return hipGetLastError();
 }
 
