@@ -18,6 +18,7 @@ struct SinglePlan {
   int kernel;     // 0: tiled (float4 rows), 1: generic, 2: tiled (unaligned rows), 3: matrix cores
   int K;
   int rows;       // output rows per lane (R)
+  int lanes;      // lanes across a tile row (64, or fewer for narrow maps; vector kernels)
   int tile_h, tile_w;
   int tiles_x, tiles_y;
   int m_per_block;

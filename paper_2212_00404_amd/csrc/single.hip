@@ -68,15 +68,24 @@ template <int K, bool VEC4> struct Occupancy { static constexpr int value = (VEC
 // the FMA loop, so they are held in VGPRs instead (one copy per lane).
 template <int K> struct FilterInVgpr { static constexpr bool value = K * K > 49; };
 
-template <int K, int R>
+// L: lanes across a row.  With L = 64 a wave covers R rows x 256 columns;
+// with L < 64 its lanes form 64 / L row groups, each R rows x 4L columns
+// (narrow maps, where most of a 256-column tile would hold no outputs).
+template <int K, int R, int L = kLanes>
 struct TileShape {
-  static constexpr int TH = kWaves * R;            // output rows per tile
+  static constexpr int RG = kLanes / L;            // row groups per wave
+  static constexpr int TW = kW * L;                // output columns per tile
+  static constexpr int TH = kWaves * RG * R;       // output rows per tile
   static constexpr int IH = TH + K - 1;            // staged input rows
   static constexpr int NQ = (kW + K - 1 + 3) / 4;  // float4 reads per lane per row
-  static constexpr int IW4 = kLanes + NQ - 1;      // float4 per staged row
+  static constexpr int IW4 = L + NQ - 1;           // float4 per staged row
   static constexpr int LW4 = IW4;                  // LDS stride of a staged row (float4)
   static constexpr int LDS = IH * LW4 * 16;
 };
+// Lanes across a row of the narrow tiles, and the widest output they serve.
+constexpr int kNarrowLanes = 16;
+constexpr int kNarrowMaxWout = 128;
+constexpr int kNarrowMaxK = 5;
 
 // s_waitcnt immediate for "vmcnt(0)" alone on gfx9-family chips: vmcnt in
 // bits 3:0 and 15:14 (0), expcnt in bits 6:4 and lgkmcnt in bits 11:8 at their
@@ -181,12 +190,12 @@ __device__ __forceinline__ void load_filter(const float *__restrict__ F, int m, 
 }
 
 // One filter over the staged tile: this lane's R x 4 outputs at (oy0, ox0).
-// NT: non-temporal output stores.
-template <int K, int R, bool NT>
+// NT: non-temporal output stores.  L: lanes across a row (TileShape).
+template <int K, int R, bool NT, int L>
 __device__ __forceinline__ void apply_filter(const float4 *rowp, const float (&f)[K][K],
                                              float *__restrict__ Om, int oy0, int ox0, int Hout,
                                              int Wout) {
-  using S = TileShape<K, R>;
+  using S = TileShape<K, R, L>;
   constexpr int IW4 = S::IW4, NQ = S::NQ;
   constexpr int G = Group<K>::value;
   static_assert(R % G == 0, "group must divide the strip");
@@ -252,11 +261,11 @@ __device__ __forceinline__ void apply_filter(const float4 *rowp, const float (&f
   }
 }
 
-template <int K, int R, bool VEC4, bool NT>
+template <int K, int R, bool VEC4, bool NT, int L>
 __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_tiled(
     const float *__restrict__ I, const float *__restrict__ F, float *__restrict__ O,
     int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block) {
-  using S = TileShape<K, R>;
+  using S = TileShape<K, R, L>;
   __shared__ float4 tile[S::IH * S::IW4];
 
   const int Hout = Wy - K + 1;
@@ -272,10 +281,14 @@ __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_ti
 
   const int lane = threadIdx.x & (kLanes - 1);
   const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x / kLanes);
-  const float4 *rowp = tile + wave * R * S::IW4 + lane;
+  // This lane's row group (first output row within the tile) and column
+  // quad.
+  const int row0 = (wave * S::RG + lane / L) * R;
+  const int cq = lane % L;
+  const float4 *rowp = tile + row0 * S::IW4 + cq;
 
   Stager<S, VEC4> st;
-  st.fetch(I, Wx, Wy, (wg / tiles_x) * S::TH, (wg % tiles_x) * kTileW);
+  st.fetch(I, Wx, Wy, (wg / tiles_x) * S::TH, (wg % tiles_x) * S::TW);
   st.commit(tile);
   lds_barrier();
 
@@ -283,15 +296,15 @@ __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_ti
   load_filter<K>(F, m_begin, f);
   for (int t = wg; t < ntiles; t += nwg) {
     const int y0 = (t / tiles_x) * S::TH;
-    const int x0 = (t % tiles_x) * kTileW;
+    const int x0 = (t % tiles_x) * S::TW;
     const int tn = t + nwg;
     const bool more = tn < ntiles;
-    if (more) st.fetch(I, Wx, Wy, (tn / tiles_x) * S::TH, (tn % tiles_x) * kTileW);
+    if (more) st.fetch(I, Wx, Wy, (tn / tiles_x) * S::TH, (tn % tiles_x) * S::TW);
 
     for (int m = m_begin; m < m_end; ++m) {
       if (m != m_begin) load_filter<K>(F, m, f);
-      apply_filter<K, R, NT>(rowp, f, O + (size_t)m * Hout * Wout, y0 + wave * R,
-                             x0 + lane * kW, Hout, Wout);
+      apply_filter<K, R, NT, L>(rowp, f, O + (size_t)m * Hout * Wout, y0 + row0,
+                                x0 + cq * kW, Hout, Wout);
     }
     if (m_end - m_begin > 1) load_filter<K>(F, m_begin, f);
 
@@ -553,12 +566,12 @@ __global__ __launch_bounds__(256) void single_generic(
 // Persistent workgroups: as many as fit on the chip at once.  Filters reuse
 // the staged tile; they are split over workgroups only as far as needed to
 // fill the chip when there are fewer tiles than slots.
-void plan_persistent(int Wx, int Wy, int K, int M, int num_cu, int th, int occupancy,
+void plan_persistent(int Wx, int Wy, int K, int M, int num_cu, int th, int tw, int occupancy,
                      SinglePlan *p) {
   const int Hout = Wy - K + 1, Wout = Wx - K + 1;
   p->tile_h = th;
-  p->tile_w = kTileW;
-  p->tiles_x = (Wout + kTileW - 1) / kTileW;
+  p->tile_w = tw;
+  p->tiles_x = (Wout + tw - 1) / tw;
   p->tiles_y = (Hout + th - 1) / th;
   const int ntiles = p->tiles_x * p->tiles_y;
   const int slots = occupancy * num_cu;
@@ -579,7 +592,18 @@ void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
   using S = TileShape<K, R>;
   p->kernel = VEC4 ? 0 : 2;
   p->rows = R;
-  plan_persistent(Wx, Wy, K, M, num_cu, S::TH, Occupancy<K, VEC4>::value, p);
+  p->lanes = kLanes;
+  if constexpr (VEC4 && K <= kNarrowMaxK) {
+    // Narrow maps: lanes in row groups over 64-column tiles.
+    if (Wx - K + 1 <= kNarrowMaxWout) {
+      using SN = TileShape<K, R, kNarrowLanes>;
+      p->lanes = kNarrowLanes;
+      plan_persistent(Wx, Wy, K, M, num_cu, SN::TH, SN::TW, Occupancy<K, VEC4>::value, p);
+      p->lds_bytes = SN::LDS;
+      return;
+    }
+  }
+  plan_persistent(Wx, Wy, K, M, num_cu, S::TH, S::TW, Occupancy<K, VEC4>::value, p);
   p->lds_bytes = S::LDS;
   if constexpr (R > kShortRows) {
     // Fewer tall tiles than compute units (a small map with few filters):
@@ -588,7 +612,7 @@ void plan_tiled(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
     if ((int64_t)p->tiles_x * p->tiles_y * p->grid_z < num_cu) {
       using SS = TileShape<K, kShortRows>;
       p->rows = kShortRows;
-      plan_persistent(Wx, Wy, K, M, num_cu, SS::TH, Occupancy<K, VEC4>::value, p);
+      plan_persistent(Wx, Wy, K, M, num_cu, SS::TH, SS::TW, Occupancy<K, VEC4>::value, p);
       p->lds_bytes = SS::LDS;
     }
   }
@@ -602,7 +626,7 @@ void plan_mfma(int Wx, int Wy, int M, int num_cu, SinglePlan *p) {
   using S = MfmaTileShape<K>;
   p->kernel = 3;
   p->rows = 8;
-  plan_persistent(Wx, Wy, K, M, num_cu, S::TH, MfmaOcc<K>::value, p);
+  plan_persistent(Wx, Wy, K, M, num_cu, S::TH, kTileW, MfmaOcc<K>::value, p);
   p->lds_bytes = S::LDS;
 }
 
@@ -630,16 +654,24 @@ template <int K, bool VEC4, int R>
 void launch_vector(const SinglePlan &p, const float *I, const float *F, float *O, int Wx, int Wy,
                    int M, bool nt, hipStream_t s) {
   const int ntiles = p.tiles_x * p.tiles_y;
-  if constexpr (K <= kTemporalMaxK) {
-    if (!nt) {
-      hipLaunchKernelGGL((single_tiled<K, R, VEC4, false>), dim3(p.grid, p.grid_z),
+  if constexpr (VEC4 && K <= kNarrowMaxK) {
+    if (p.lanes == kNarrowLanes) {
+      hipLaunchKernelGGL((single_tiled<K, R, VEC4, true, kNarrowLanes>), dim3(p.grid, p.grid_z),
                          dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles,
                          p.m_per_block);
       return;
     }
   }
-  hipLaunchKernelGGL((single_tiled<K, R, VEC4, true>), dim3(p.grid, p.grid_z), dim3(kBlock), 0,
-                     s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block);
+  if constexpr (K <= kTemporalMaxK) {
+    if (!nt) {
+      hipLaunchKernelGGL((single_tiled<K, R, VEC4, false, kLanes>), dim3(p.grid, p.grid_z),
+                         dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles,
+                         p.m_per_block);
+      return;
+    }
+  }
+  hipLaunchKernelGGL((single_tiled<K, R, VEC4, true, kLanes>), dim3(p.grid, p.grid_z),
+                     dim3(kBlock), 0, s, I, F, O, Wx, Wy, M, p.tiles_x, ntiles, p.m_per_block);
 }
 
 template <int K>
