@@ -209,3 +209,49 @@ def test_split_calls_on_two_streams():
         O64, _ = oracle_multi(*data[k])
         for o in outs[k]:
             assert_exact(o.cpu().numpy(), O64, "stream %d" % k)
+
+
+def test_calls_from_several_host_threads():
+    """Four host threads, each with its own stream, issue channel-split and
+    single-map calls at once (the C calls run without the Python lock): the
+    per-(device, stream) workspaces and the planner are shared state, and
+    every result must still be exact."""
+    import threading
+
+    shapes = [(512, 512, 9, 9, 3), (256, 256, 30, 30, 3), (512, 512, 16, 16, 3),
+              (256, 256, 28, 28, 1)]
+    assert all(dc.plan_multi(*s)["split_c"] > 1 for s in shapes)
+    data = [random_arrays(*s, seed=9200 + i, variant="int") for i, s in enumerate(shapes)]
+    Is, Fs = random_arrays(1, 3, 300, 200, 5, seed=9300, variant="int")
+    dev = torch.device("cuda:0")
+    inputs = [(torch.from_numpy(I).to(dev), torch.from_numpy(F).to(dev)) for I, F in data]
+    single_in = (torch.from_numpy(Is[0]).to(dev), torch.from_numpy(Fs[:, 0]).to(dev))
+    torch.cuda.synchronize()
+    outs = [[] for _ in shapes]
+    errors = []
+
+    def worker(k):
+        try:
+            torch.cuda.set_device(dev)
+            s = torch.cuda.Stream()
+            with torch.cuda.stream(s):
+                for _ in range(8):
+                    outs[k].append((dc.multi(*inputs[k]), dc.single(*single_in)))
+            s.synchronize()
+        except Exception as e:  # reported below, on the main thread
+            errors.append(repr(e))
+
+    threads = [threading.Thread(target=worker, args=(k,)) for k in range(len(shapes))]
+    for t in threads:
+        t.start()
+    for t in threads:
+        t.join()
+    torch.cuda.synchronize()
+    assert not errors, errors
+    O64s, _ = oracle_single(Is[0], Fs[:, 0])
+    for k, (I, F) in enumerate(data):
+        O64, _ = oracle_multi(I, F)
+        assert len(outs[k]) == 8
+        for om, osg in outs[k]:
+            assert_exact(om.cpu().numpy(), O64, "thread %d multi" % k)
+            assert_exact(osg.cpu().numpy(), O64s, "thread %d single" % k)
