@@ -1,7 +1,7 @@
 """GPU: every multi-channel plan the library can run (each workgroup shape
 crossed with each channel split, both kernel families) against the oracle,
 plans chosen by the caller, and the latency probe behind the paper's model.
-Integer data, so every plan must be bit-exact (SURVEY reading: every
+Integer data, so every plan must be bit-exact (every
 summation order of small integers is exact in fp32)."""
 import numpy as np
 import pytest
