@@ -85,7 +85,7 @@ int oracle_conv_f64(const float *I, const float *F, int C, int M, int Wx,
   return 0;
 }
 
-/* Number of OpenMP threads this build can use (1 without OpenMP). */
+/* Number of OpenMP threads available to this library (1 when compiled without OpenMP). */
 int oracle_max_threads(void) {
 #ifdef _OPENMP
   return omp_get_max_threads();
