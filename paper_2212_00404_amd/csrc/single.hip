@@ -3,9 +3,11 @@
 // One input map I[Wy][Wx], M filters F[M][K][K], output O[M][Hout][Wout].
 //
 // Design for gfx950 (the paper's SM partitioning for Pascal is prior art):
-//  * The output is cut into TH x 256 tiles (TH = 4 waves x R rows).  A tile
-//    needs its input rows plus K-1 halo rows and columns (Section 3.1 adds the
-//    same K-1 extra lines to each map piece).
+//  * The output is cut into TH x 256 tiles (TH = 4 waves x R rows; R = 4 or 8,
+//    4 where tall tiles would leave compute units idle), or for outputs up to
+//    128 columns wide into 64-column tiles whose waves split into four row
+//    groups.  A tile needs its input rows plus K-1 halo rows and columns
+//    (Section 3.1 adds the same K-1 extra lines to each map piece).
 //  * Workgroups are persistent: each walks every nwg-th tile and, while it
 //    computes one tile from LDS, the global loads of its next tile are
 //    already in flight into registers (the prefetching of Section 2.2,
@@ -21,6 +23,8 @@
 //  * The filters of a workgroup (its share of the M filters) are applied to
 //    each staged tile in turn, so the map is read from HBM once per filter
 //    group (the map-split method of Section 3.1).
+//  * Each lane writes its 4 columns of a row with one 16-byte store at any
+//    row alignment, non-temporal except in one case chosen on the host.
 #include <type_traits>
 
 #include "internal.h"
