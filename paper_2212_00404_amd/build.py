@@ -34,10 +34,33 @@ CFLAGS = [
 ]
 
 
+def _code_only(text: str) -> str:
+    """C/C++ source without its comments, trailing blanks and empty lines."""
+    out, i, n = [], 0, len(text)
+    while i < n:
+        c = text[i]
+        if c in "\"'":
+            j = i + 1
+            while j < n and text[j] != c:
+                j += 2 if text[j] == "\\" else 1
+            out.append(text[i:j + 1])
+            i = j + 1
+        elif text.startswith("//", i):
+            j = text.find("\n", i)
+            i = n if j < 0 else j
+        elif text.startswith("/*", i):
+            j = text.find("*/", i + 2)
+            i = n if j < 0 else j + 2
+        else:
+            out.append(c)
+            i += 1
+    return "\n".join(l.rstrip() for l in "".join(out).splitlines() if l.strip())
+
+
 def source_digest(names=None) -> str:
-    """SHA-256 over kernel sources (identifies a kernel build).  ``names``:
-    file names under ``csrc/`` to cover (default: every source and the ABI
-    header)."""
+    """SHA-256 over the code of the kernel sources, comments excluded
+    (identifies what is compiled).  ``names``: file names under ``csrc/`` to
+    cover (default: every source and the ABI header)."""
     import hashlib
     h = hashlib.sha256()
     if names is None:
@@ -46,8 +69,8 @@ def source_digest(names=None) -> str:
         files = [os.path.join(CSRC, n) for n in names]
     for f in files:
         h.update(os.path.basename(f).encode())
-        with open(f, "rb") as fh:
-            h.update(fh.read())
+        with open(f, encoding="utf-8") as fh:
+            h.update(_code_only(fh.read()).encode())
     return h.hexdigest()[:16]
 
 

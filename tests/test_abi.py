@@ -206,3 +206,14 @@ def test_multi_plan_random(shape):
     for v in ("auto", "valu") + (("mfma",) if shape[4] <= 7 else ()):
         _check_multi_plan(*shape, variant=v)
 
+
+
+def test_source_digest_ignores_comments_only():
+    """The digest that ties recorded HBM counters to a kernel build covers the
+    code, not its comments."""
+    from paper_2212_00404_amd.build import _code_only
+    a = "int f(int x) { return x + 1; }  // one\n/* two */\n"
+    b = "/* header */\nint f(int x) { return x + 1; }\n\n"
+    assert _code_only(a) == _code_only(b)
+    assert _code_only('s = "//kept";') == 's = "//kept";'
+    assert _code_only("x = 1;") != _code_only("x = 2;")
