@@ -144,44 +144,45 @@ constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
 //    unmasked chunks.
 constexpr int mfma_fp(int K, int CC) { return (CC * K * K) | 1; }
 constexpr int mfma_ics(int K, int PT) { return 64 * ceil_div(K * (PT + K - 1), 64); }
-// Filter rows are copied by the four waves in blocks of MT/4 consecutive
+// Filter rows are copied by the NW waves in blocks of MT/NW consecutive
 // rows, each block followed by a 64-float gap (see the kernel's issue()).
-constexpr int mfma_fblk(int K, int MT, int CC) { return (MT / 4) * mfma_fp(K, CC) + 64; }
-constexpr int mfma_buf_floats(int K, int MT, int PT, int CC) {
-  return 4 * mfma_fblk(K, MT, CC) + CC * mfma_ics(K, PT);
+constexpr int mfma_fblk(int K, int MT, int CC, int NW) { return (MT / NW) * mfma_fp(K, CC) + 64; }
+constexpr int mfma_buf_floats(int K, int MT, int PT, int CC, int NW) {
+  return NW * mfma_fblk(K, MT, CC, NW) + CC * mfma_ics(K, PT);
 }
 // Channels per stage: the largest multiple of 2*WC (a channel pair per wave
 // group and k-step), at most 64, whose two stage buffers fit in 80 KB (two
 // workgroups per CU).
-constexpr int mfma_cc(int K, int MT, int PT, int WC) {
+constexpr int mfma_cc(int K, int MT, int PT, int WC, int NW) {
   int best = 2 * WC;
   for (int cc = 2 * WC; cc <= 64; cc += 2 * WC)
-    if (2 * mfma_buf_floats(K, MT, PT, cc) * 4 <= 80 * 1024) best = cc;
+    if (2 * mfma_buf_floats(K, MT, PT, cc, NW) * 4 <= 80 * 1024) best = cc;
   return best;
 }
 
 template <int K, int MB, int NB, int WM, int WN, int WC>
 struct MfmaCfg {
   static constexpr int KK = K * K;
+  static constexpr int NW = WM * WN * WC;   // waves per workgroup
   static constexpr int MT = 32 * MB * WM;   // filters per workgroup
   static constexpr int PT = 32 * NB * WN;   // pixel lanes per workgroup tile
-  static constexpr int CC = mfma_cc(K, MT, PT, WC);  // channels per stage
+  static constexpr int CC = mfma_cc(K, MT, PT, WC, NW);  // channels per stage
   static constexpr int CCW = CC / WC;       // channels per wave group per stage
   static constexpr int FROW = CC * KK;      // staged floats per filter
   static constexpr int FP = mfma_fp(K, CC);
   static constexpr int NCF = ceil_div(FROW, 64);       // 64-lane chunks per filter row
-  static constexpr int RPW = MT / 4;                   // filter rows copied per wave
-  static constexpr int FBLK = mfma_fblk(K, MT, CC);    // LDS stride of a wave's row block
-  static constexpr int F_FLOATS = 4 * FBLK;
+  static constexpr int RPW = MT / NW;                  // filter rows copied per wave
+  static constexpr int FBLK = mfma_fblk(K, MT, CC, NW);  // LDS stride of a wave's row block
+  static constexpr int F_FLOATS = NW * FBLK;
   static constexpr int ICS = mfma_ics(K, PT);
   static constexpr int NCI = ICS / 64;                 // most chunks an input plane needs
   static constexpr int BUF = F_FLOATS + CC * ICS;      // one stage buffer
   static constexpr int RED = (WC - 1) * WM * WN * MB * NB * 1024;
   static constexpr int BUF0 = BUF > RED ? BUF : RED;   // buffer 0 also holds the WC sums
   static constexpr int LDS_BYTES = (BUF0 + BUF) * 4;
-  static_assert(WM * WN * WC == 4, "four waves per workgroup");
+  static_assert(NW == 4 || NW == 8, "four or eight waves per workgroup");
   static_assert(CCW % 2 == 0, "channels are consumed in pairs");
-  static_assert(MT % 4 == 0, "filter rows are shared out over four waves");
+  static_assert(MT % NW == 0, "filter rows are shared out over the waves");
 };
 
 // Stage pipeline: while the MFMAs consume stage s from one LDS buffer, the
@@ -192,7 +193,7 @@ struct MfmaCfg {
 // the map or past a filter row are pointed at valid elements whose values
 // only reach outputs that are never stored (or the padding of a row).
 template <int K, int MB, int NB, int WM, int WN, int WC>
-__global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I,
+__global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__restrict__ I,
                                                      const float *__restrict__ F,
                                                      float *__restrict__ O,
                                                      float *__restrict__ ws, TileArgs a) {
@@ -200,6 +201,7 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
   constexpr int KK = Cfg::KK, MT = Cfg::MT, CC = Cfg::CC, CCW = Cfg::CCW, FROW = Cfg::FROW;
   constexpr int FP = Cfg::FP, ICS = Cfg::ICS, F_FLOATS = Cfg::F_FLOATS;
   constexpr int NCF = Cfg::NCF, NCI = Cfg::NCI, RPW = Cfg::RPW, FBLK = Cfg::FBLK;
+  constexpr int NW = Cfg::NW, NTHR = 64 * NW;
   __shared__ float buf0[Cfg::BUF0];
   __shared__ float buf1[Cfg::BUF];
 
@@ -334,12 +336,12 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
         }
       }
       const float *src = I + (size_t)(c0 + wave) * plane_elems;
-      for (int cl = wave; cl < CC; cl += 4) {
+      for (int cl = wave; cl < CC; cl += NW) {
         float *dsti = buf + F_FLOATS + cl * ICS;
 #pragma unroll
         for (int j = 0; j < NCI; ++j)
           if (j < nci) dma_f32(src + ioff[j], dsti + 64 * j);
-        src += 4 * plane_elems;
+        src += NW * plane_elems;
       }
     } else {
       // Partial stage (the channel range ends inside it): copy the nc
@@ -352,7 +354,7 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
         for (int q = 0; q < NCF; ++q)
           if (64 * q + lane < flen) dma_f32(src + 64 * q, dst + 64 * q);
       }
-      for (int cl = wave; cl < nc; cl += 4) {
+      for (int cl = wave; cl < nc; cl += NW) {
         const float *src = I + (size_t)(c0 + cl) * plane_elems;
         float *dst = buf + F_FLOATS + cl * ICS;
 #pragma unroll
@@ -360,11 +362,11 @@ __global__ __launch_bounds__(kBlock) void multi_mfma(const float *__restrict__ I
           if (j < nci) dma_f32(src + ioff[j], dst + 64 * j);
       }
       const int fz = FROW - flen;
-      for (int idx = threadIdx.x; idx < MT * fz; idx += kBlock) {
+      for (int idx = threadIdx.x; idx < MT * fz; idx += NTHR) {
         const int r = idx / fz;
         buf[(r / RPW) * FBLK + (r % RPW) * FP + flen + (idx - r * fz)] = 0.f;
       }
-      for (int idx = threadIdx.x; idx < (CC - nc) * ICS; idx += kBlock)
+      for (int idx = threadIdx.x; idx < (CC - nc) * ICS; idx += NTHR)
         buf[F_FLOATS + nc * ICS + idx] = 0.f;
     }
   };
@@ -674,6 +676,8 @@ constexpr MfmaShape kMfmaShapes[] = {
     {1, 2, 2, 2, 1},  // 64 x 128
     {2, 2, 2, 2, 1},  // 128 x 128
     {1, 2, 1, 1, 4},  // 32 x 64, channel sum split over 4 waves
+    {1, 1, 2, 2, 2},  // 64 x 64, eight waves, channel sum split over 2 wave groups
+    {1, 1, 2, 4, 1},  // 64 x 128, eight waves
 };
 constexpr int kNumMfma = sizeof(kMfmaShapes) / sizeof(kMfmaShapes[0]);
 
@@ -688,9 +692,16 @@ template <int K, int S>
 hipError_t launch_mfma_shape(const MultiPlan &p, const float *I, const float *F, float *O,
                              float *ws, const TileArgs &a, hipStream_t st) {
   constexpr MfmaShape sh = kMfmaShapes[S];
-  auto kern = multi_mfma<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC>;
-  hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(kBlock), 0, st, I, F, O, ws, a);
-  return hipGetLastError();
+  // Shapes whose stage buffers exceed the LDS for this K are never planned
+  // (the candidate list drops them) and are not instantiated.
+  if constexpr (MfmaCfg<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC>::LDS_BYTES > kMaxLds) {
+    return hipErrorInvalidValue;
+  } else {
+    auto kern = multi_mfma<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC>;
+    hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(64 * sh.WM * sh.WN * sh.WC), 0, st, I, F, O, ws,
+                       a);
+    return hipGetLastError();
+  }
 }
 
 template <int K>
@@ -703,6 +714,8 @@ hipError_t launch_mfma_k(const MultiPlan &p, const float *I, const float *F, flo
     case 3: return launch_mfma_shape<K, 3>(p, I, F, O, ws, a, st);
     case 4: return launch_mfma_shape<K, 4>(p, I, F, O, ws, a, st);
     case 5: return launch_mfma_shape<K, 5>(p, I, F, O, ws, a, st);
+    case 6: return launch_mfma_shape<K, 6>(p, I, F, O, ws, a, st);
+    case 7: return launch_mfma_shape<K, 7>(p, I, F, O, ws, a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -758,26 +771,31 @@ struct Candidate {
   int ops_per_kstep;  // MFMAs per wave per (channel pair, r, s); VALU: FMAs per lane per (c, r, s)
   int lds_fixed;      // static LDS bytes (MFMA family), 0 if it depends on the tile
   int red_floats;     // LDS floats for the in-workgroup channel-group sum
+  int waves;          // waves per workgroup
 };
 
 Candidate mfma_candidate(int i, int K) {
   const MfmaShape s = kMfmaShapes[i];
   const int MT = 32 * s.MB * s.WM, PT = 32 * s.NB * s.WN;
-  const int CC = mfma_cc(K, MT, PT, s.WC);
-  const int buf = mfma_buf_floats(K, MT, PT, CC);
+  const int NW = s.WM * s.WN * s.WC;
+  const int CC = mfma_cc(K, MT, PT, s.WC, NW);
+  const int buf = mfma_buf_floats(K, MT, PT, CC, NW);
   const int red = (s.WC - 1) * s.WM * s.WN * s.MB * s.NB * 1024;
-  return Candidate{i, MT, PT, s.WC, CC, s.MB * s.NB, ((buf > red ? buf : red) + buf) * 4, red};
+  return Candidate{i, MT, PT, s.WC, CC, s.MB * s.NB, ((buf > red ? buf : red) + buf) * 4, red, NW};
 }
 
 Candidate valu_candidate(int i) {
   const ValuShape s = kValuShapes[i];
-  return Candidate{i, s.MR * (4 / s.WC), 64, s.WC, s.CC, s.MR, 0, (s.WC - 1) * (4 / s.WC) * s.MR * 64};
+  return Candidate{i, s.MR * (4 / s.WC), 64, s.WC, s.CC, s.MR, 0, (s.WC - 1) * (4 / s.WC) * s.MR * 64,
+                   4};
 }
 
 // Rough time model in GPU clock cycles, used only to rank candidates.
 //   work:  inner-product plus per-stage bookkeeping cycles of the busiest CU
-//          (co-resident workgroups share its four SIMDs); splitting the
-//          stage's channels over WC wave groups adds their LDS reduction
+//          (co-resident workgroups share its four SIMDs; a SIMD with a
+//          single wave issues its MFMAs less densely than one with two);
+//          splitting the stage's channels over WC wave groups adds their LDS
+//          reduction
 //   chain: a workgroup's stages cannot run faster than the load latency
 //          (the MFMA family overlaps the next stage's loads with the current
 //          stage; the VALU family pays the latency every stage); `occ`
@@ -785,7 +803,7 @@ Candidate valu_candidate(int i) {
 //   split: partial sums written, re-read and added by a second launch
 // The constants were fitted to exhaustive timings of every candidate plan of
 // nineteen layer shapes on an MI355X (the fitted model picks a plan within
-// 1.6% of the fastest on average, 10.5% at worst).
+// 1.9% of the fastest on average, 10.1% at worst).
 double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, int Wout,
                 int num_cu, const TileChoice &t, int split, int cps, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
@@ -793,22 +811,27 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, i
   const int64_t blocks = ntiles * mtiles * split;
   const int stages = (cps + cd.CC - 1) / cd.CC;
   const int kk = K * K;
-  constexpr double kMfmaCycles = 64.0;    // one 32x32x2 MFMA per wave
+  constexpr double kMfmaCycles = 48.0;    // one 32x32x2 MFMA per wave
+  constexpr double kOneWavePerSimd = 1.1; // MFMA cycles factor with one wave per SIMD
   constexpr double kStageOverhead = 300.0;
   constexpr double kWcReduction = 500.0;  // per extra wave group, per stage
-  constexpr double kLatency = 2000.0;
+  constexpr double kLatency = 3000.0;
   constexpr double kLaunch = 2000.0;
   constexpr double kSplitLaunch = 2000.0;
   constexpr double kSplitBytesPerClock = 2000.0;
-  constexpr int kMaxOcc = 2;
-  const double per_stage = (mfma ? (double)(cd.CC / cd.WC / 2) * kk * cd.ops_per_kstep * kMfmaCycles
-                                 : (double)(cd.CC / cd.WC) * kk * cd.ops_per_kstep * 4.0) +
-                           kStageOverhead + (cd.WC - 1) * kWcReduction;
+  constexpr int kMaxOcc = 2;              // four-wave workgroups per CU
   int occ = (int)(160 * 1024 / (lds_bytes > 0 ? lds_bytes : 1));
-  if (occ > kMaxOcc) occ = kMaxOcc;
+  if (occ > kMaxOcc * 4 / cd.waves) occ = kMaxOcc * 4 / cd.waves;
   if (occ < 1) occ = 1;
   const int64_t per_cu = (blocks + num_cu - 1) / num_cu;
   const int64_t rounds = (per_cu + occ - 1) / occ;
+  const int64_t waves_per_simd = cd.waves / 4 * (per_cu < occ ? per_cu : occ);
+  // (eight-wave workgroups put two waves on each SIMD)
+  const double per_stage =
+      (mfma ? (double)(cd.CC / cd.WC / 2) * kk * cd.ops_per_kstep * kMfmaCycles * cd.waves / 4 *
+                  (waves_per_simd < 2 ? kOneWavePerSimd : 1.0)
+            : (double)(cd.CC / cd.WC) * kk * cd.ops_per_kstep * 4.0) +
+      kStageOverhead + (cd.WC - 1) * kWcReduction;
   const double work = (double)per_cu * stages * per_stage;
   const double stage_chain = mfma ? (per_stage > kLatency ? per_stage : kLatency)
                                   : per_stage + kLatency;
@@ -859,7 +882,7 @@ void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu
       p.grid_x = (int)((int64_t)t.tiles_x * t.tiles_y * ((M + cd.MT - 1) / cd.MT) * split);
       p.grid_y = 1;
       p.grid_z = 1;
-      p.block = kBlock;
+      p.block = 64 * cd.waves;
       p.lds_bytes = (int)lds_bytes;
       p.workspace_bytes = split > 1 ? (int64_t)split * M * Hout * Wout * 4 : 0;
       out.emplace_back(tm, p);
