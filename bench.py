@@ -227,12 +227,35 @@ def cpu_baseline(launches, reps, min_seconds=10.0):
                 oracle.conv_multi(I, F, threads=threads)
         times.append(time.perf_counter() - t0)
     best = min(times)
+    # the same step on one thread, once (context: the oracle's per-core rate)
+    t0 = time.perf_counter()
+    for w, I, F in launches:
+        if w.kind == "single":
+            oracle.conv_single(I, F, threads=1)
+        else:
+            oracle.conv_multi(I, F, threads=1)
+    one = time.perf_counter() - t0
     return {"value": round(flops / best / 1e9, 3), "unit": "GFLOP/s", "cores": threads,
             "kind": "oracle",
             "sample": "whole steps (%d launch%s, %.2f GFLOP each), %d repetitions in %.1f s, "
                       "fastest reported, fp64 C oracle"
                       % (len(launches), "es" if len(launches) > 1 else "", flops / 1e9,
-                         len(times), sum(times))}
+                         len(times), sum(times)),
+            "single_thread_value": round(flops / one / 1e9, 3),
+            "affinity_cpus": len(os.sched_getaffinity(0)),
+            "cpu_model": _cpu_model()}
+
+
+def _cpu_model():
+    """The host CPU's model name (what lscpu prints), or None."""
+    try:
+        with open("/proc/cpuinfo") as fh:
+            for line in fh:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return None
 
 
 def miopen_context(bufs, per_kernel, steps, warmup):
