@@ -498,6 +498,22 @@ def main():
             "frac_fp32_peak": round(tf / PEAK_FP32_VECTOR_TFLOPS, 4),
             "frac_hbm": round(gbs / PEAK_HBM_GBS, 4)})
 
+    # Warm figures: each launch repeated back to back on the same buffers
+    # (working sets up to the 256 MB Infinity Cache stay resident), events
+    # only around the repeats.  The step above rotates through separate
+    # buffers and measures the cold case.
+    reps = max(1, min(args.steps, 20))
+    for i, b in enumerate(bufs):
+        launch(b)
+        torch.cuda.synchronize()
+        a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(stream)
+        for _ in range(reps):
+            launch(b)
+        z.record(stream)
+        torch.cuda.synchronize()
+        per_kernel[i]["back_to_back_us"] = round(a.elapsed_time(z) / reps * 1e3, 2)
+
     if args.miopen:
         miopen_context(bufs, per_kernel, args.steps, args.warmup)
 

@@ -14,7 +14,8 @@ from gpu_util import assert_exact, oracle_multi
 pytestmark = pytest.mark.gpu
 
 LAYERS = [(33, 70, 23, 19, 3), (130, 7, 9, 9, 3), (64, 64, 7, 7, 7), (16, 40, 30, 30, 5),
-          (8, 33, 12, 12, 1), (5, 9, 20, 17, 2)]
+          (8, 33, 12, 12, 1), (5, 9, 20, 17, 2), (20, 65, 15, 13, 4), (12, 70, 14, 16, 6),
+          (40, 130, 40, 36, 3)]
 
 
 @pytest.mark.parametrize("layer", LAYERS, ids=[str(l) for l in LAYERS])
