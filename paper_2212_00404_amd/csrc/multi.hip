@@ -152,7 +152,8 @@ constexpr int mfma_buf_floats(int K, int MT, int PT, int CC, int NW) {
 }
 // Channels per stage: the largest multiple of 2*WC (a channel pair per wave
 // group and k-step), at most 64, whose two stage buffers fit in 80 KB (two
-// workgroups per CU).
+// four-wave workgroups per CU; an eight-wave workgroup fills a CU's SIMDs
+// with two waves each on its own, and longer stages measured no faster).
 constexpr int mfma_cc(int K, int MT, int PT, int WC, int NW) {
   int best = 2 * WC;
   for (int cc = 2 * WC; cc <= 64; cc += 2 * WC)
