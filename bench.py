@@ -507,6 +507,7 @@ def main():
         launch(b)
         torch.cuda.synchronize()
         a, z = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        gpu_delay()
         a.record(stream)
         for _ in range(reps):
             launch(b)
