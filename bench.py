@@ -63,7 +63,7 @@ def parse():
                          "one JSON line per footprint and stride")
     ap.add_argument("--miopen", action="store_true",
                     help="also time torch.nn.functional.conv2d (MIOpen on ROCm, fp32 with "
-                         "TF32 disabled) on each multi-channel workload of the step, as "
+                         "TF32 disabled) on each workload of the step, as "
                          "context beside each kernel's time")
     ap.add_argument("--autotune", action="store_true",
                     help="for the multi-channel workload(s), time every candidate plan, the "
@@ -260,8 +260,8 @@ def _cpu_model():
 
 def miopen_context(bufs, per_kernel, steps, warmup):
     """torch's own convolution (MIOpen) on the same inputs: a context figure
-    for each multi-channel workload, not a parity reference.  Eq. 1 is what
-    conv2d computes with no padding, stride 1 and weights [M][C][K][K]."""
+    for each workload, not a parity reference.  Eq. 1 is what conv2d computes
+    with no padding, stride 1 and weights [M][C][K][K] (Eq. 2: C = 1)."""
     import torch
     import paper_2212_00404_amd as dc
     torch.backends.cudnn.allow_tf32 = False
@@ -272,6 +272,12 @@ def miopen_context(bufs, per_kernel, steps, warmup):
             fn()
         torch.cuda.synchronize()
         a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        # a GPU-side delay first, so that the launches queue up behind it and
+        # short kernels are timed back to back, not at the host's launch rate
+        try:
+            torch.cuda._sleep(int(min(0.2, 5e-5 * steps) * 2.0e9))
+        except (AttributeError, RuntimeError):
+            pass
         a.record()
         for _ in range(steps):
             fn()
@@ -280,14 +286,17 @@ def miopen_context(bufs, per_kernel, steps, warmup):
         return a.elapsed_time(b) / steps * 1e3
 
     for i, (w, It, Ft, Ot) in enumerate(bufs):
-        if w.kind != "multi":
-            continue
-        x = It[None]
-        ref = torch.nn.functional.conv2d(x, Ft)
-        us = back_to_back(lambda: torch.nn.functional.conv2d(x, Ft))
+        if w.kind == "multi":
+            x, wt = It[None], Ft
+            run = lambda: dc.multi(It, Ft, out=Ot)
+        else:
+            x, wt = It[None, None], Ft[:, None]
+            run = lambda: dc.single(It, Ft, out=Ot)
+        ref = torch.nn.functional.conv2d(x, wt)
+        us = back_to_back(lambda: torch.nn.functional.conv2d(x, wt))
         # libdconv timed the same way (the same layer back to back, events
         # only around the run), so the two figures are comparable
-        ours = back_to_back(lambda: dc.multi(It, Ft, out=Ot))
+        ours = back_to_back(run)
         diff = (ref[0] - Ot).abs().max().item()
         scale = Ot.abs().max().item() or 1.0
         per_kernel[i]["miopen_us"] = round(us, 2)
