@@ -141,9 +141,12 @@ constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
 //  * Input planes: ICS floats per channel = the largest (tpy+K-1)*(tpx+K-1)
 //    over output tiles of at most PT pixels, K*(PT+K-1) (a 1 x PT or PT x 1
 //    tile), rounded up to whole 64-lane chunks so a plane is copied with
-//    unmasked chunks.
+//    unmasked chunks; planes of at most 32 floats (K = 1, 32-pixel tiles)
+//    take 32, and one 64-lane copy then fills two channels.
 constexpr int mfma_fp(int K, int CC) { return (CC * K * K) | 1; }
-constexpr int mfma_ics(int K, int PT) { return 64 * ceil_div(K * (PT + K - 1), 64); }
+constexpr int mfma_ics(int K, int PT) {
+  return K * (PT + K - 1) <= 32 ? 32 : 64 * ceil_div(K * (PT + K - 1), 64);
+}
 // Filter rows are copied by the NW waves in blocks of MT/NW consecutive
 // rows, each block followed by a 64-float gap (see the kernel's issue()).
 constexpr int mfma_fblk(int K, int MT, int CC, int NW) { return (MT / NW) * mfma_fp(K, CC) + 64; }
@@ -154,20 +157,29 @@ constexpr int mfma_buf_floats(int K, int MT, int PT, int CC, int NW) {
 // group and k-step), at most 64, whose two stage buffers fit in 80 KB (two
 // four-wave workgroups per CU; an eight-wave workgroup fills a CU's SIMDs
 // with two waves each on its own, and longer stages measured no faster).
-constexpr int mfma_cc(int K, int MT, int PT, int WC, int NW) {
+//   A deep shape instead takes the largest power-of-two multiple of 2*WC, up
+// to 256 channels, whose two buffers fit in 160 KB (one workgroup per CU):
+// for small tiles with little work per channel (K = 1), where each stage
+// costs about one load latency whatever its size.
+constexpr int mfma_cc(int K, int MT, int PT, int WC, int NW, bool DEEP) {
   int best = 2 * WC;
+  if (DEEP) {
+    for (int cc = 2 * WC; cc <= 256; cc *= 2)
+      if (2 * mfma_buf_floats(K, MT, PT, cc, NW) * 4 <= 160 * 1024) best = cc;
+    return best;
+  }
   for (int cc = 2 * WC; cc <= 64; cc += 2 * WC)
     if (2 * mfma_buf_floats(K, MT, PT, cc, NW) * 4 <= 80 * 1024) best = cc;
   return best;
 }
 
-template <int K, int MB, int NB, int WM, int WN, int WC>
+template <int K, int MB, int NB, int WM, int WN, int WC, bool DEEP>
 struct MfmaCfg {
   static constexpr int KK = K * K;
   static constexpr int NW = WM * WN * WC;   // waves per workgroup
   static constexpr int MT = 32 * MB * WM;   // filters per workgroup
   static constexpr int PT = 32 * NB * WN;   // pixel lanes per workgroup tile
-  static constexpr int CC = mfma_cc(K, MT, PT, WC, NW);  // channels per stage
+  static constexpr int CC = mfma_cc(K, MT, PT, WC, NW, DEEP);  // channels per stage
   static constexpr int CCW = CC / WC;       // channels per wave group per stage
   static constexpr int FROW = CC * KK;      // staged floats per filter
   static constexpr int FP = mfma_fp(K, CC);
@@ -176,7 +188,8 @@ struct MfmaCfg {
   static constexpr int FBLK = mfma_fblk(K, MT, CC, NW);  // LDS stride of a wave's row block
   static constexpr int F_FLOATS = NW * FBLK;
   static constexpr int ICS = mfma_ics(K, PT);
-  static constexpr int NCI = ICS / 64;                 // most chunks an input plane needs
+  static constexpr bool PAIR = ICS == 32;              // two input planes per 64-lane copy
+  static constexpr int NCI = PAIR ? 1 : ICS / 64;      // most chunks an input plane needs
   static constexpr int BUF = F_FLOATS + CC * ICS;      // one stage buffer
   static constexpr int RED = (WC - 1) * WM * WN * MB * NB * 1024;
   static constexpr int BUF0 = BUF > RED ? BUF : RED;   // buffer 0 also holds the WC sums
@@ -193,16 +206,17 @@ struct MfmaCfg {
 // full stage is issued as unmasked 64-lane copies: lanes that fall outside
 // the map or past a filter row are pointed at valid elements whose values
 // only reach outputs that are never stored (or the padding of a row).
-template <int K, int MB, int NB, int WM, int WN, int WC>
+template <int K, int MB, int NB, int WM, int WN, int WC, bool DEEP>
 __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__restrict__ I,
                                                      const float *__restrict__ F,
                                                      float *__restrict__ O,
                                                      float *__restrict__ ws, TileArgs a) {
-  using Cfg = MfmaCfg<K, MB, NB, WM, WN, WC>;
+  using Cfg = MfmaCfg<K, MB, NB, WM, WN, WC, DEEP>;
   constexpr int KK = Cfg::KK, MT = Cfg::MT, CC = Cfg::CC, CCW = Cfg::CCW, FROW = Cfg::FROW;
   constexpr int FP = Cfg::FP, ICS = Cfg::ICS, F_FLOATS = Cfg::F_FLOATS;
   constexpr int NCF = Cfg::NCF, NCI = Cfg::NCI, RPW = Cfg::RPW, FBLK = Cfg::FBLK;
   constexpr int NW = Cfg::NW, NTHR = 64 * NW;
+  constexpr bool PAIR = Cfg::PAIR;
   __shared__ float buf0[Cfg::BUF0];
   __shared__ float buf1[Cfg::BUF];
 
@@ -253,13 +267,15 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 
   // Per-lane source offsets of one input plane, chunk j covers plane elements
   // [64j, 64j+64): element e is row e / IW, column e % IW of the halo tile,
-  // clamped into the map.
+  // clamped into the map.  PAIR: one chunk covers two planes, lanes 0-31
+  // element e = lane of the first and lanes 32-63 element lane - 32 of the
+  // next channel (one map further).
   const int plane = a.IH * a.IW;
-  const int nci = (plane + 63) >> 6;
+  const int nci = PAIR ? 1 : (plane + 63) >> 6;
   int ioff[NCI];
 #pragma unroll
   for (int j = 0; j < NCI; ++j) {
-    int e = 64 * j + lane;
+    int e = PAIR ? (lane & 31) : 64 * j + lane;
     if (e >= plane) e = 0;
     const int iy = e / a.IW;
     const int gy = min(py0 + iy, a.Wy - 1);
@@ -276,6 +292,8 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   // re-read the row's first element.  Otherwise the last chunk is masked.
   constexpr bool FSPILL = 64 * NCF <= 2 * FP;
   const size_t plane_elems = (size_t)a.Wy * a.Wx;
+  // PAIR: lanes 32-63 copy the next channel's plane
+  const size_t pair_off = PAIR ? (size_t)(lane >> 5) * plane_elems : 0;
   const size_t frow_stride = (size_t)a.C * KK;
   const int e_last = 64 * (NCF - 1) + lane;
   const bool f_spill = e_last >= FROW;
@@ -336,13 +354,22 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
           dst += FP;
         }
       }
-      const float *src = I + (size_t)(c0 + wave) * plane_elems;
-      for (int cl = wave; cl < CC; cl += NW) {
-        float *dsti = buf + F_FLOATS + cl * ICS;
+      if constexpr (PAIR) {
+        // channel pairs (cl, cl + 1), cl even; CC is even
+        const float *src = I + (size_t)(c0 + 2 * wave) * plane_elems;
+        for (int cl = 2 * wave; cl < CC; cl += 2 * NW) {
+          dma_f32(src + pair_off + ioff[0], buf + F_FLOATS + cl * ICS);
+          src += 2 * NW * plane_elems;
+        }
+      } else {
+        const float *src = I + (size_t)(c0 + wave) * plane_elems;
+        for (int cl = wave; cl < CC; cl += NW) {
+          float *dsti = buf + F_FLOATS + cl * ICS;
 #pragma unroll
-        for (int j = 0; j < NCI; ++j)
-          if (j < nci) dma_f32(src + ioff[j], dsti + 64 * j);
-        src += NW * plane_elems;
+          for (int j = 0; j < NCI; ++j)
+            if (j < nci) dma_f32(src + ioff[j], dsti + 64 * j);
+          src += NW * plane_elems;
+        }
       }
     } else {
       // Partial stage (the channel range ends inside it): copy the nc
@@ -355,12 +382,20 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
         for (int q = 0; q < NCF; ++q)
           if (64 * q + lane < flen) dma_f32(src + 64 * q, dst + 64 * q);
       }
-      for (int cl = wave; cl < nc; cl += NW) {
-        const float *src = I + (size_t)(c0 + cl) * plane_elems;
-        float *dst = buf + F_FLOATS + cl * ICS;
+      if constexpr (PAIR) {
+        // the second plane of the last pair only where that channel exists
+        for (int cl = 2 * wave; cl < nc; cl += 2 * NW)
+          if (cl + (lane >> 5) < nc)
+            dma_f32(I + (size_t)(c0 + cl) * plane_elems + pair_off + ioff[0],
+                    buf + F_FLOATS + cl * ICS);
+      } else {
+        for (int cl = wave; cl < nc; cl += NW) {
+          const float *src = I + (size_t)(c0 + cl) * plane_elems;
+          float *dst = buf + F_FLOATS + cl * ICS;
 #pragma unroll
-        for (int j = 0; j < NCI; ++j)
-          if (j < nci) dma_f32(src + ioff[j], dst + 64 * j);
+          for (int j = 0; j < NCI; ++j)
+            if (j < nci) dma_f32(src + ioff[j], dst + 64 * j);
+        }
       }
       const int fz = FROW - flen;
       for (int idx = threadIdx.x; idx < MT * fz; idx += NTHR) {
@@ -669,16 +704,17 @@ hipError_t allow_full_lds(Kern kern) {
 // Kernel table
 // ---------------------------------------------------------------------------
 // Each family has a few workgroup shapes; the planner picks one per call.
-struct MfmaShape { int MB, NB, WM, WN, WC; };
+struct MfmaShape { int MB, NB, WM, WN, WC; bool deep; };
 constexpr MfmaShape kMfmaShapes[] = {
-    {1, 1, 2, 1, 2},  // 64 filters x 32 pixels, channel sum split over 2 wave pairs
-    {1, 2, 1, 2, 2},  // 32 x 128, channel sum split over 2 wave pairs
-    {1, 1, 2, 2, 1},  // 64 x 64
-    {1, 2, 2, 2, 1},  // 64 x 128
-    {2, 2, 2, 2, 1},  // 128 x 128
-    {1, 2, 1, 1, 4},  // 32 x 64, channel sum split over 4 waves
-    {1, 1, 2, 2, 2},  // 64 x 64, eight waves, channel sum split over 2 wave groups
-    {1, 1, 2, 4, 1},  // 64 x 128, eight waves
+    {1, 1, 2, 1, 2, false},  // 64 filters x 32 pixels, channel sum split over 2 wave pairs
+    {1, 2, 1, 2, 2, false},  // 32 x 128, channel sum split over 2 wave pairs
+    {1, 1, 2, 2, 1, false},  // 64 x 64
+    {1, 2, 2, 2, 1, false},  // 64 x 128
+    {2, 2, 2, 2, 1, false},  // 128 x 128
+    {1, 2, 1, 1, 4, false},  // 32 x 64, channel sum split over 4 waves
+    {1, 1, 2, 2, 2, false},  // 64 x 64, eight waves, channel sum split over 2 wave groups
+    {1, 1, 2, 4, 1, false},  // 64 x 128, eight waves
+    {1, 1, 1, 1, 4, true},   // 32 x 32, channel sum split over 4 waves, deep stages
 };
 constexpr int kNumMfma = sizeof(kMfmaShapes) / sizeof(kMfmaShapes[0]);
 
@@ -695,10 +731,10 @@ hipError_t launch_mfma_shape(const MultiPlan &p, const float *I, const float *F,
   constexpr MfmaShape sh = kMfmaShapes[S];
   // Shapes whose stage buffers exceed the LDS for this K are never planned
   // (the candidate list drops them) and are not instantiated.
-  if constexpr (MfmaCfg<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC>::LDS_BYTES > kMaxLds) {
+  if constexpr (MfmaCfg<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC, sh.deep>::LDS_BYTES > kMaxLds) {
     return hipErrorInvalidValue;
   } else {
-    auto kern = multi_mfma<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC>;
+    auto kern = multi_mfma<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC, sh.deep>;
     hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(64 * sh.WM * sh.WN * sh.WC), 0, st, I, F, O, ws,
                        a);
     return hipGetLastError();
@@ -717,6 +753,7 @@ hipError_t launch_mfma_k(const MultiPlan &p, const float *I, const float *F, flo
     case 5: return launch_mfma_shape<K, 5>(p, I, F, O, ws, a, st);
     case 6: return launch_mfma_shape<K, 6>(p, I, F, O, ws, a, st);
     case 7: return launch_mfma_shape<K, 7>(p, I, F, O, ws, a, st);
+    case 8: return launch_mfma_shape<K, 8>(p, I, F, O, ws, a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -779,7 +816,7 @@ Candidate mfma_candidate(int i, int K) {
   const MfmaShape s = kMfmaShapes[i];
   const int MT = 32 * s.MB * s.WM, PT = 32 * s.NB * s.WN;
   const int NW = s.WM * s.WN * s.WC;
-  const int CC = mfma_cc(K, MT, PT, s.WC, NW);
+  const int CC = mfma_cc(K, MT, PT, s.WC, NW, s.deep);
   const int buf = mfma_buf_floats(K, MT, PT, CC, NW);
   const int red = (s.WC - 1) * s.WM * s.WN * s.MB * s.NB * 1024;
   return Candidate{i, MT, PT, s.WC, CC, s.MB * s.NB, ((buf > red ? buf : red) + buf) * 4, red, NW};
@@ -804,7 +841,7 @@ Candidate valu_candidate(int i) {
 //   split: partial sums written, re-read and added by a second launch
 // The constants were fitted to exhaustive timings of every candidate plan of
 // nineteen layer shapes on an MI355X (the fitted model picks a plan within
-// 1.9% of the fastest on average, 10.1% at worst).
+// about 1% of the fastest on average, 7% at worst).
 double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, int Wout,
                 int num_cu, const TileChoice &t, int split, int cps, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
@@ -812,14 +849,14 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, i
   const int64_t blocks = ntiles * mtiles * split;
   const int stages = (cps + cd.CC - 1) / cd.CC;
   const int kk = K * K;
-  constexpr double kMfmaCycles = 48.0;    // one 32x32x2 MFMA per wave
-  constexpr double kOneWavePerSimd = 1.1; // MFMA cycles factor with one wave per SIMD
-  constexpr double kStageOverhead = 300.0;
+  constexpr double kMfmaCycles = 80.0;    // one 32x32x2 MFMA per wave (issue: 64)
+  constexpr double kOneWavePerSimd = 1.3; // MFMA cycles factor with one wave per SIMD
+  constexpr double kStageOverhead = 1200.0;
   constexpr double kWcReduction = 500.0;  // per extra wave group, per stage
-  constexpr double kLatency = 3000.0;
+  constexpr double kLatency = 5000.0;
   constexpr double kLaunch = 2000.0;
-  constexpr double kSplitLaunch = 2000.0;
-  constexpr double kSplitBytesPerClock = 2000.0;
+  constexpr double kSplitLaunch = 5000.0;
+  constexpr double kSplitBytesPerClock = 1000.0;
   constexpr int kMaxOcc = 2;              // four-wave workgroups per CU
   int occ = (int)(160 * 1024 / (lds_bytes > 0 ? lds_bytes : 1));
   if (occ > kMaxOcc * 4 / cd.waves) occ = kMaxOcc * 4 / cd.waves;

@@ -219,7 +219,7 @@ def test_calls_from_several_host_threads():
     import threading
 
     shapes = [(512, 512, 9, 9, 3), (256, 256, 30, 30, 3), (512, 512, 16, 16, 3),
-              (256, 256, 28, 28, 1)]
+              (512, 512, 14, 14, 1)]
     assert all(dc.plan_multi(*s)["split_c"] > 1 for s in shapes)
     data = [random_arrays(*s, seed=9200 + i, variant="int") for i, s in enumerate(shapes)]
     Is, Fs = random_arrays(1, 3, 300, 200, 5, seed=9300, variant="int")

@@ -15,7 +15,7 @@ pytestmark = pytest.mark.gpu
 
 LAYERS = [(33, 70, 23, 19, 3), (130, 7, 9, 9, 3), (64, 64, 7, 7, 7), (16, 40, 30, 30, 5),
           (8, 33, 12, 12, 1), (5, 9, 20, 17, 2), (20, 65, 15, 13, 4), (12, 70, 14, 16, 6),
-          (40, 130, 40, 36, 3)]
+          (40, 130, 40, 36, 3), (7, 40, 10, 9, 1), (67, 33, 31, 29, 1)]
 
 
 @pytest.mark.parametrize("layer", LAYERS, ids=[str(l) for l in LAYERS])
