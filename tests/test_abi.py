@@ -187,6 +187,14 @@ def test_mfma_refuses_large_filters():
         dc.plan_multi(4, 4, 20, 20, 9, "mfma")
 
 
+def test_split_test_shapes_still_split():
+    """The GPU tests of the channel-split machinery need plans that split."""
+    import split_shapes
+    for s in split_shapes.THREADS + split_shapes.TWO_STREAMS:
+        assert dc.plan_multi(*s)["split_c"] > 1, s
+    assert sum(dc.plan_multi(*s)["split_c"] > 1 for s in split_shapes.REUSE) >= 3
+
+
 def test_small_maps_split_the_channel_sum():
     """7x7 outputs with 512 channels give far fewer tiles than compute units:
     the planner must split the channel sum across workgroups."""

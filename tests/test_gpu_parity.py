@@ -11,6 +11,7 @@ import pytest
 import torch
 
 import paper_2212_00404_amd as dc
+import split_shapes
 from dconv_workloads import WORKLOADS, make, random_arrays
 from gpu_util import (assert_exact, assert_within, gpu_multi, gpu_single, oracle_multi,
                       oracle_single)
@@ -175,8 +176,7 @@ def test_split_workspace_reused_across_plans():
     back to back on one stream share its workspace: the arrival counters must
     be back at zero after every call, and growth between calls must not
     disturb queued work."""
-    shapes = [(512, 512, 9, 9, 3), (256, 256, 30, 30, 3), (64, 96, 20, 20, 3),
-              (512, 512, 9, 9, 3), (128, 128, 60, 60, 5), (256, 256, 28, 28, 1)]
+    shapes = split_shapes.REUSE
     splits = [dc.plan_multi(*s)["split_c"] for s in shapes]
     assert sum(sp > 1 for sp in splits) >= 3, splits
     cases = []
@@ -193,7 +193,7 @@ def test_split_workspace_reused_across_plans():
 
 def test_split_calls_on_two_streams():
     """Concurrent channel-split calls on two streams use separate workspaces."""
-    shapes = [(512, 512, 9, 9, 3), (512, 512, 16, 16, 3)]
+    shapes = split_shapes.TWO_STREAMS
     assert all(dc.plan_multi(*s)["split_c"] > 1 for s in shapes)
     data = [random_arrays(*s, seed=9100 + i, variant="int") for i, s in enumerate(shapes)]
     dev = [(torch.from_numpy(I).cuda(), torch.from_numpy(F).cuda()) for I, F in data]
@@ -218,8 +218,7 @@ def test_calls_from_several_host_threads():
     every result must still be exact."""
     import threading
 
-    shapes = [(512, 512, 9, 9, 3), (256, 256, 30, 30, 3), (512, 512, 16, 16, 3),
-              (512, 512, 14, 14, 1)]
+    shapes = split_shapes.THREADS
     assert all(dc.plan_multi(*s)["split_c"] > 1 for s in shapes)
     data = [random_arrays(*s, seed=9200 + i, variant="int") for i, s in enumerate(shapes)]
     Is, Fs = random_arrays(1, 3, 300, 200, 5, seed=9300, variant="int")
