@@ -849,14 +849,16 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, i
   const int64_t blocks = ntiles * mtiles * split;
   const int stages = (cps + cd.CC - 1) / cd.CC;
   const int kk = K * K;
+  // Fitted per family: the matrix-core kernels on every layer with their
+  // eight-wave and deep shapes, the vector kernels on the same layers.
   constexpr double kMfmaCycles = 80.0;    // one 32x32x2 MFMA per wave (issue: 64)
   constexpr double kOneWavePerSimd = 1.3; // MFMA cycles factor with one wave per SIMD
-  constexpr double kStageOverhead = 1200.0;
   constexpr double kWcReduction = 500.0;  // per extra wave group, per stage
-  constexpr double kLatency = 5000.0;
   constexpr double kLaunch = 2000.0;
-  constexpr double kSplitLaunch = 5000.0;
-  constexpr double kSplitBytesPerClock = 1000.0;
+  const double kStageOverhead = mfma ? 1200.0 : 300.0;
+  const double kLatency = mfma ? 5000.0 : 2000.0;
+  const double kSplitLaunch = mfma ? 5000.0 : 2000.0;
+  const double kSplitBytesPerClock = mfma ? 1000.0 : 2000.0;
   constexpr int kMaxOcc = 2;              // four-wave workgroups per CU
   int occ = (int)(160 * 1024 / (lds_bytes > 0 ? lds_bytes : 1));
   if (occ > kMaxOcc * 4 / cd.waves) occ = kMaxOcc * 4 / cd.waves;
