@@ -574,6 +574,11 @@ def main():
         "higher_is_better": True, "scaling": "weak", "vs_baseline": None, "dtype": "f32",
         "data": "synthetic", "config": config, "roofline": roof, "cpu_baseline": cpu,
         "per_kernel": per_kernel, "wall_s_timed": round(wall, 4),
+        # The paper's own speedups over cuDNN v7.1 on a Pascal GPU (Section 4):
+        # context only, another library on another machine.
+        "paper_context": {"speedup_vs_cudnn_pascal": {
+            "single_channel": {"average": 2.6, "range": [1.5, 5.6]},
+            "multi_channel": {"average": 1.39, "range": [1.05, 2.0]}}},
     }
     print(json.dumps(out), flush=True)
 
