@@ -65,6 +65,10 @@ def parse():
                     help="also time torch.nn.functional.conv2d (MIOpen on ROCm, fp32 with "
                          "TF32 disabled) on each workload of the step, as "
                          "context beside each kernel's time")
+    ap.add_argument("--heldout", type=int, default=0, metavar="N",
+                    help="time every matrix-core candidate plan of N seeded random layer shapes "
+                         "(not the ones the planner's model was fitted on) and the planner's "
+                         "choice; one JSON line per shape")
     ap.add_argument("--autotune", action="store_true",
                     help="for the multi-channel workload(s), time every candidate plan, the "
                          "planner's choice and the paper-rule choice; one JSON line per workload")
@@ -128,6 +132,59 @@ def autotune(names, steps, warmup):
             "planner": planner, "planner_us": us(planner),
             "paper_rule": paper, "paper_rule_us": us(paper),
             "model": dc.model_latency(dc.MI355X), "us": times}), flush=True)
+
+
+def heldout(n, steps, warmup, seed=20221230):
+    """The planner on layer shapes it was not fitted on: C, M in 32..512,
+    outputs 7..112 square, K in {1, 3, 5, 7} (at most 3 GFLOP each), drawn
+    from a seeded generator; every matrix-core candidate plan timed over
+    `steps` back-to-back launches behind a GPU-side delay."""
+    import torch
+    import paper_2212_00404_amd as dc
+    rng = np.random.default_rng(seed)
+    dev = torch.device("cuda:0")
+    shapes = []
+    while len(shapes) < n:
+        K = int(rng.choice([1, 3, 5, 7]))
+        hout = int(rng.choice([7, 12, 14, 20, 28, 40, 56, 80, 112]))
+        C = int(rng.choice([32, 64, 96, 128, 192, 256, 384, 512]))
+        M = int(rng.choice([32, 64, 96, 128, 192, 256, 384, 512]))
+        if 2 * C * M * K * K * hout * hout <= 6e9:
+            shapes.append((C, M, hout + K - 1, hout + K - 1, K))
+
+    def tag(p):
+        return "k%d/m%d/%dx%d/c%d/s%d" % (p["kernel"], p["tile_m"], p["tile_h"], p["tile_w"],
+                                         p["chunk_c"], p["split_c"])
+
+    g = torch.Generator(device=dev)
+    g.manual_seed(seed)
+    for (C, M, Wx, Wy, K) in shapes:
+        I = torch.rand((C, Wy, Wx), device=dev, generator=g)
+        F = torch.randn((M, C, K, K), device=dev, generator=g) * (2.0 / (C * K * K)) ** 0.5
+        O = torch.empty((M, Wy - K + 1, Wx - K + 1), device=dev)
+        times = {}
+        for p in dc.plan_multi_candidates(C, M, Wx, Wy, K, "mfma"):
+            for _ in range(max(1, warmup)):
+                dc.multi(I, F, out=O, plan=p)
+            torch.cuda.synchronize()
+            try:
+                torch.cuda._sleep(int(min(0.2, 6e-5 * steps) * 2.0e9))
+            except (AttributeError, RuntimeError):
+                pass
+            a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            a.record()
+            for _ in range(steps):
+                dc.multi(I, F, out=O, plan=p)
+            b.record()
+            torch.cuda.synchronize()
+            times[tag(p)] = a.elapsed_time(b) / steps * 1e3
+        planner = tag(dc.plan_multi(C, M, Wx, Wy, K))
+        best = min(times, key=times.get)
+        print(json.dumps({"shape": {"C": C, "M": M, "Wx": Wx, "Wy": Wy, "K": K},
+                          "candidates": len(times), "best": best, "best_us": round(times[best], 2),
+                          "planner": planner, "planner_us": round(times[planner], 2),
+                          "planner_over_best": round(times[planner] / times[best], 3)}),
+              flush=True)
 
 
 def copy_probe(mib, steps):
@@ -387,6 +444,9 @@ def main():
         return
     if args.latency_probe:
         latency_probe()
+        return
+    if args.heldout:
+        heldout(args.heldout, args.steps, args.warmup)
         return
     if args.autotune:
         from dconv_workloads import WORKLOADS
