@@ -47,7 +47,8 @@ def parse():
                     help="%s (default), %s, %s, %s, or a name from dconv_workloads.WORKLOADS"
                          % SWEEPS)
     ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "valu"],
-                    help="kernel family for multi-channel workloads")
+                    help="kernel family: multi-channel workloads; for the single map, "
+                         "mfma runs the matrix-core kernel where it exists (K = 5 ... 11)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--cpu-reps", type=int, default=2)
     ap.add_argument("--ingest-pmc", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
@@ -490,10 +491,14 @@ def main():
         bufs.append((w, It, Ft, Ot))
     torch.cuda.synchronize()
 
+    def single_variant(w):
+        # the matrix-core single-map kernel exists for K = 5 ... 11
+        return args.variant if args.variant != "mfma" or 5 <= w.K <= 11 else "auto"
+
     def launch(b):
         w, It, Ft, Ot = b
         if w.kind == "single":
-            dc.single(It, Ft, out=Ot)
+            dc.single(It, Ft, out=Ot, variant=single_variant(w))
         else:
             dc.multi(It, Ft, out=Ot, variant=args.variant)
 
@@ -591,10 +596,13 @@ def main():
     w = bufs[dom][0]
     pk = per_kernel[dom]
     ridge_unpacked = PEAK_FP32_UNPACKED_TFLOPS * 1e12 / (PEAK_HBM_GBS * 1e9)
-    uses_mfma = (w.kind == "multi" and
-                 dc.plan_multi(w.C, w.M, w.Wx, w.Wy, w.K, args.variant)["variant"] == 2)
+    if w.kind == "multi":
+        uses_mfma = dc.plan_multi(w.C, w.M, w.Wx, w.Wy, w.K, args.variant)["variant"] == 2
+    else:
+        uses_mfma = dc.plan_single(w.Wx, w.Wy, w.K, w.M, variant=single_variant(w))["variant"] == 2
     compute_bound = (w.flops / w.compulsory_bytes) >= ridge_unpacked
-    traffic = traffic_for(w.name) if w.kind == "single" else None
+    # the recorded HBM counters belong to the vector kernels of the single map
+    traffic = traffic_for(w.name) if w.kind == "single" and not uses_mfma else None
     if compute_bound:
         achieved = w.flops / (pk["avg_us"] * 1e-6) / 1e12
         peak = PEAK_FP32_MFMA_TFLOPS if uses_mfma else PEAK_FP32_VECTOR_TFLOPS
@@ -616,7 +624,7 @@ def main():
 
     if args.workload == SWEEP:
         config = {"workload": SWEEP, "kind": "single", "Wx": 4096, "Wy": 4096, "M": 1, "C": 1,
-                  "K": [3, 5, 7, 9, 11], "launches_per_step": 5,
+                  "K": [3, 5, 7, 9, 11], "launches_per_step": 5, "variant": args.variant,
                   "buffers": "separate I/O per K (670 MB per step)"}
     elif args.workload in sweeps:
         config = {"workload": args.workload, "kind": bufs[0][0].kind,
