@@ -58,6 +58,10 @@ def parse():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="instead of convolving, copy a MIB-sized device buffer --steps "
                          "times (reference kernel for scaling HBM byte counters)")
+    ap.add_argument("--peaks", action="store_true",
+                    help="instead of convolving, run the peak microbenchmarks (HBM read, write "
+                         "and copy streams, fp32 FMA, fp32 MFMA 32x32x2 and 16x16x4, global->LDS "
+                         "copies of 4 and 16 bytes per lane); one JSON line")
     ap.add_argument("--latency-probe", action="store_true",
                     help="instead of convolving, measure dependent-load latency over chains of "
                          "64 KiB to 4 GiB (the latency input of the paper's partition model); "
@@ -86,7 +90,7 @@ def latency_probe():
 
 def autotune(names, steps, warmup):
     """Per multi-channel workload: the time of every candidate plan (both
-    kernel families, every workgroup shape and channel split), of the
+    kernel families, every workgroup shape), of the
     planner's choice and of the plan the paper's Section 3.2 rules pick for
     an MI355X.  Each plan is timed over `steps` back-to-back launches."""
     import torch
@@ -118,8 +122,8 @@ def autotune(names, steps, warmup):
 
         def tag(p):
             fam = "mfma" if p["variant"] == 2 else "valu"
-            return "%s/k%d/m%d/%dx%d/c%d/s%d" % (fam, p["kernel"], p["tile_m"], p["tile_h"],
-                                                p["tile_w"], p["chunk_c"], p["split_c"])
+            return "%s/k%d/m%d/%dx%d/c%d/w%d" % (fam, p["kernel"], p["tile_m"], p["tile_h"],
+                                                p["tile_w"], p["chunk_c"], p["waves_c"])
 
         cands = dc.plan_multi_candidates(*args)
         times = {tag(p): round(timed(p), 2) for p in cands}
@@ -154,8 +158,8 @@ def heldout(n, steps, warmup, seed=20221230):
             shapes.append((C, M, hout + K - 1, hout + K - 1, K))
 
     def tag(p):
-        return "k%d/m%d/%dx%d/c%d/s%d" % (p["kernel"], p["tile_m"], p["tile_h"], p["tile_w"],
-                                         p["chunk_c"], p["split_c"])
+        return "k%d/m%d/%dx%d/c%d/w%d" % (p["kernel"], p["tile_m"], p["tile_h"], p["tile_w"],
+                                         p["chunk_c"], p["waves_c"])
 
     g = torch.Generator(device=dev)
     g.manual_seed(seed)
@@ -445,6 +449,10 @@ def main():
         return
     if args.latency_probe:
         latency_probe()
+        return
+    if args.peaks:
+        from paper_2212_00404_amd import peaks
+        print(json.dumps({"peaks": peaks.run()}), flush=True)
         return
     if args.heldout:
         heldout(args.heldout, args.steps, args.warmup)

@@ -31,9 +31,12 @@
  *     pointers never touch the device.
  *   - Results are accumulated in fp32 in a fixed order for a given shape and
  *     device, so repeated calls give bitwise identical output.
+ *   - The library allocates no device memory and needs no workspace: every
+ *     call reads and writes the caller's three tensors only (and the latency
+ *     probe its own two arguments).
  *   - Calls on different streams may run concurrently; the library keeps no
  *     state that two calls share except an immutable per-device property
- *     cache and the per-(device, stream) workspace of dconv_multi.
+ *     cache (compute-unit counts, read once).
  *   - Nothing is printed and the library never aborts.
  */
 #ifndef DCONV_H
@@ -50,7 +53,6 @@ extern "C" {
 #define DCONV_ERANGE (-3)       /* a tensor has more than 2^31-1 elements */
 #define DCONV_EHIP (-4)         /* the HIP runtime reported an error */
 #define DCONV_EUNSUPPORTED (-5) /* the forced variant cannot run this shape */
-#define DCONV_ENOMEM (-6)       /* a stream-ordered workspace could not be allocated */
 
 /* Kernel families for the *_variant calls and the plans. */
 #define DCONV_VARIANT_AUTO 0 /* the planner's choice */
@@ -86,13 +88,10 @@ int dconv_single_variant(const float *I, const float *F, float *O, int Wx, int W
  *   I : device, C*Wy*Wx floats    F : device, M*C*K*K floats
  *   O : device, M*(Wy-K+1)*(Wx-K+1) floats, written
  *   note the argument order (C, M, Wx, Wy, K) differs from dconv_single
- * When the planner splits the channel sum across workgroups the partial
- * sums go to a workspace the library keeps per (device, stream): it is taken
- * from the device's default memory pool with a stream-ordered allocation the
- * first time a stream needs it (or needs more), reused by later calls on that
- * stream, and kept until the process ends; DCONV_ENOMEM if the allocation
- * fails.  The partial sums are added in a fixed order, so results stay
- * deterministic.  Other returns as for dconv_single.
+ * The channel sum of every output stays inside one workgroup (Section 2.3
+ * rejects dividing it over processors); where a workgroup's waves split a
+ * stage's channels, their partial sums are added through LDS in a fixed
+ * order, so results are deterministic.  Returns as for dconv_single.
  */
 int dconv_multi(const float *I, const float *F, float *O, int C, int M, int Wx,
                 int Wy, int K, void *stream);
@@ -112,8 +111,8 @@ const char *dconv_strerror(int status);
 /*
  * Launch plan, as chosen by the planner (host logic only, no device access).
  * Paper, Section 2.3 and Section 3: the work is divided among compute units
- * along the filters (m), along the map (x, y) and, for maps too small to fill
- * the chip, along the channels with a fixed-order sum of the partial results.
+ * along the filters (m) and along the map (x, y); the channel sum of an
+ * output is never divided among workgroups, only among the waves of one.
  */
 typedef struct dconv_plan {
   int variant;          /* DCONV_VARIANT_VALU or DCONV_VARIANT_MFMA */
@@ -121,11 +120,11 @@ typedef struct dconv_plan {
   int tile_m;           /* filters per workgroup */
   int tile_h, tile_w;   /* output rows and columns per workgroup tile */
   int chunk_c;          /* channels staged in LDS per pipeline step */
-  int split_c;          /* channel groups summed across workgroups (1: none) */
+  int waves_c;          /* wave groups of a workgroup that split each stage's
+                           channels (their sums added through LDS; 1: none) */
   int grid_x, grid_y, grid_z;
   int block;            /* threads per workgroup */
   int lds_bytes;        /* LDS per workgroup */
-  long long workspace_bytes; /* stream-ordered scratch (0: none) */
 } dconv_plan;
 
 /*
@@ -143,9 +142,8 @@ int dconv_plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_c
 /*
  * dconv_plan_multi_candidates -- every plan of a kernel family (both
  * families for DCONV_VARIANT_AUTO) that fits a device with `num_cu` compute
- * units: each workgroup shape crossed with each channel split, in a fixed
- * order.  dconv_plan_multi returns one of them (the planner's estimate is the
- * smallest).  Writes min(count, capacity) plans to `out` (may be NULL when
+ * units: each workgroup shape, in a fixed order.  dconv_plan_multi returns
+ * one of them (the planner's estimate is the smallest).  Writes min(count, capacity) plans to `out` (may be NULL when
  * capacity is 0) and the total to *count.  For autotuning (Section 3 divides
  * the work by rules; these are the alternatives the rules choose from).
  */
@@ -156,7 +154,7 @@ int dconv_plan_multi_candidates(int C, int M, int Wx, int Wy, int K, int variant
  * dconv_multi_with_plan -- dconv_multi with a plan chosen by the caller, which
  * must equal (field by field) one of the candidates dconv_plan_multi_candidates
  * returns for these sizes on the current device; DCONV_EINVAL otherwise.
- * Semantics, workspace and returns as for dconv_multi.
+ * Semantics and returns as for dconv_multi.
  */
 int dconv_multi_with_plan(const float *I, const float *F, float *O, int C, int M, int Wx,
                           int Wy, int K, const dconv_plan *plan, void *stream);

@@ -5,9 +5,7 @@
 // so NULL pointers and bad sizes are reported without a device.
 #include <climits>
 #include <cstdint>
-#include <map>
 #include <mutex>
-#include <utility>
 #include <vector>
 
 #include "internal.h"
@@ -45,21 +43,6 @@ int current_num_cu(int *num_cu) {
   return DCONV_OK;
 }
 
-// Workspace for partial sums of a split channel sum, one per (device,
-// stream).  Calls on one stream run in stream order and may share it; calls
-// on different streams get different buffers.  A buffer only grows: the old
-// one is released with a stream-ordered free (after the work already queued
-// on that stream) and a larger one taken from the device's default pool.
-// The lock is held until the kernels that use the buffer are enqueued, so a
-// concurrent growth on the same stream is ordered after them.  Buffers live
-// until the process ends.
-struct Workspace {
-  void *ptr = nullptr;
-  size_t bytes = 0;
-};
-std::mutex g_ws_mu;
-std::map<std::pair<int, hipStream_t>, Workspace> g_ws;
-
 // Sizes of Eq. 1: C, M, K >= 1, 1 <= K <= min(Wx, Wy) (valid mode needs at
 // least one output), and every tensor indexable with 32-bit element offsets.
 int validate_sizes(int C, int M, int Wx, int Wy, int K) {
@@ -81,13 +64,12 @@ void export_single(const dconv::SinglePlan &p, dconv_plan *out) {
   out->tile_h = p.tile_h;
   out->tile_w = p.tile_w;
   out->chunk_c = 1;
-  out->split_c = 1;
+  out->waves_c = 1;
   out->grid_x = p.grid;
   out->grid_y = p.grid_z;
   out->grid_z = 1;
   out->block = p.block;
   out->lds_bytes = p.lds_bytes;
-  out->workspace_bytes = 0;
 }
 
 
@@ -107,6 +89,9 @@ DCONV_EXPORT int dconv_single_variant(const float *I, const float *F, float *O, 
   rc = dconv::plan_single(Wx, Wy, K, M, num_cu, (reinterpret_cast<uintptr_t>(I) & 15) == 0,
                           variant, &p);
   if (rc != DCONV_OK) return rc;
+  // A launch error still pending from earlier work in this thread is
+  // cleared first, so DCONV_EHIP reports this call's launch only.
+  (void)hipGetLastError();
   const hipError_t e = dconv::launch_single(p, I, F, O, Wx, Wy, M, (hipStream_t)stream);
   return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
 }
@@ -118,47 +103,21 @@ DCONV_EXPORT int dconv_single(const float *I, const float *F, float *O, int Wx, 
 
 namespace {
 
-// Launch a multi-channel plan, with the stream's workspace when it splits
-// the channel sum.
+// Launch a multi-channel plan.  A launch error still pending from earlier
+// work in this thread is cleared first, so DCONV_EHIP reports this call's
+// launch only.
 int run_multi(const dconv::MultiPlan &p, const float *I, const float *F, float *O, int C, int M,
               int Wx, int Wy, hipStream_t st) {
-  if (p.workspace_bytes == 0) {
-    const hipError_t e = dconv::launch_multi(p, I, F, O, nullptr, C, M, Wx, Wy, st);
-    return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
-  }
-  int dev = 0;
-  if (hipGetDevice(&dev) != hipSuccess) {
-    (void)hipGetLastError();
-    return DCONV_EHIP;
-  }
-  std::lock_guard<std::mutex> lock(g_ws_mu);
-  Workspace &w = g_ws[std::make_pair(dev, st)];
-  if (w.bytes < (size_t)p.workspace_bytes) {
-    if (w.ptr && hipFreeAsync(w.ptr, st) != hipSuccess) {
-      (void)hipGetLastError();
-      return DCONV_EHIP;
-    }
-    w.ptr = nullptr;
-    w.bytes = 0;
-    const size_t want = (size_t)p.workspace_bytes;
-    if (hipMallocAsync(&w.ptr, want, st) != hipSuccess) {
-      (void)hipGetLastError();
-      w.ptr = nullptr;
-      return DCONV_ENOMEM;
-    }
-    w.bytes = want;
-  }
-  const hipError_t e =
-      dconv::launch_multi(p, I, F, O, static_cast<float *>(w.ptr), C, M, Wx, Wy, st);
+  (void)hipGetLastError();
+  const hipError_t e = dconv::launch_multi(p, I, F, O, C, M, Wx, Wy, st);
   return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
 }
 
 bool same_plan(const dconv_plan &a, const dconv_plan &b) {
   return a.variant == b.variant && a.kernel == b.kernel && a.tile_m == b.tile_m &&
          a.tile_h == b.tile_h && a.tile_w == b.tile_w && a.chunk_c == b.chunk_c &&
-         a.split_c == b.split_c && a.grid_x == b.grid_x && a.grid_y == b.grid_y &&
-         a.grid_z == b.grid_z && a.block == b.block && a.lds_bytes == b.lds_bytes &&
-         a.workspace_bytes == b.workspace_bytes;
+         a.waves_c == b.waves_c && a.grid_x == b.grid_x && a.grid_y == b.grid_y &&
+         a.grid_z == b.grid_z && a.block == b.block && a.lds_bytes == b.lds_bytes;
 }
 
 }  // namespace
@@ -230,7 +189,6 @@ DCONV_EXPORT const char *dconv_strerror(int status) {
     case DCONV_ERANGE: return "a tensor has more than 2^31-1 elements";
     case DCONV_EHIP: return "the HIP runtime reported an error";
     case DCONV_EUNSUPPORTED: return "the requested kernel family cannot run this shape";
-    case DCONV_ENOMEM: return "workspace allocation failed";
     default: return "unknown status";
   }
 }

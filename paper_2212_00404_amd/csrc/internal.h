@@ -51,12 +51,10 @@ struct MultiPlan {
   int tpy, tpx;   // output tile rows x cols per workgroup
   int tiles_x, tiles_y;
   int chunk_c;    // channels per LDS stage
-  int split_c;    // workgroups along the channel sum
-  int c_per_split;
+  int waves_c;    // wave groups splitting the channel sum inside a workgroup
   int grid_x, grid_y, grid_z;
   int block;
   int lds_bytes;
-  int64_t workspace_bytes;
 };
 
 int plan_multi(int C, int M, int Wx, int Wy, int K, int variant, int num_cu, MultiPlan *p);
@@ -66,7 +64,7 @@ int multi_candidates(int C, int M, int Wx, int Wy, int K, int variant, int num_c
                      std::vector<MultiPlan> &out);
 // The public description of a plan.
 void export_multi_plan(const MultiPlan &p, dconv_plan *out);
-hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, float *O,
-                        float *ws, int C, int M, int Wx, int Wy, hipStream_t s);
+hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, float *O, int C,
+                        int M, int Wx, int Wy, hipStream_t s);
 
 }  // namespace dconv

@@ -33,6 +33,7 @@ __global__ __launch_bounds__(64) void chase(const int *__restrict__ chain, int s
 DCONV_EXPORT int dconv_probe_latency(const int *chain, int steps, long long *out, void *stream) {
   if (!chain || !out) return DCONV_ENULL;
   if (steps < 1) return DCONV_EINVAL;
+  (void)hipGetLastError();  // report this launch only
   hipLaunchKernelGGL(chase, dim3(1), dim3(64), 0, (hipStream_t)stream, chain, steps, out);
   return hipGetLastError() == hipSuccess ? DCONV_OK : DCONV_EHIP;
 }

@@ -169,13 +169,12 @@ DCONV_EXPORT int dconv_plan_multi_paper(int C, int M, int Wx, int Wy, int K,
   double best_work = -1.0;
   for (int i = 0; i < (int)all.size(); ++i) {
     const dconv::MultiPlan &p = all[i];
-    if (p.split_c != 1) continue;
     const int64_t per_wg = (int64_t)p.tile_m * p.chunk_c * K * K * p.tpy * p.tpx;
     // Co-resident workgroups: as many as the on-chip memory holds, at most
-    // kMaxWgPerCu (2048 threads per compute unit in workgroups of 256).
-    constexpr int64_t kMaxWgPerCu = 8;
-    int64_t occ = p.lds_bytes > 0 ? dev->onchip_bytes / p.lds_bytes : kMaxWgPerCu;
-    if (occ > kMaxWgPerCu) occ = kMaxWgPerCu;
+    // 2048 threads per compute unit.
+    const int64_t max_wg = 2048 / p.block;
+    int64_t occ = p.lds_bytes > 0 ? dev->onchip_bytes / p.lds_bytes : max_wg;
+    if (occ > max_wg) occ = max_wg;
     if (occ < 1) occ = 1;
     const int64_t wgs_per_cu = (p.grid_x + dev->num_cu - 1) / dev->num_cu;
     if (occ > wgs_per_cu) occ = wgs_per_cu;

@@ -13,20 +13,20 @@
 // needs), re-sized for gfx950's 160 KB LDS and 64-wide waves.
 //
 // Maps of 7x7 or 14x14 pixels give far fewer output tiles than the 256
-// compute units, so the channel sum is also split: inside a workgroup across
-// its waves (added through LDS in a fixed order), and, when that is still too
-// little work, across workgroups (partial sums to a workspace, added by a
-// second kernel in a fixed order).  The paper rejects a cross-SM channel
-// split because of the extra global traffic; on gfx950 the traffic is small
-// next to leaving most compute units idle, and it is used only when the
-// planner's estimate says so.
+// compute units.  As the paper does (Section 2.3 rejects dividing the channel
+// sum over processors: extra global traffic and synchronisation), the sum
+// stays inside one workgroup: small maps take small tiles (16 filters x 16
+// pixels) and up to 16 waves per workgroup, each wave summing its own share
+// of every stage's channels; the shares are added through LDS in a fixed
+// order.  The library needs no device memory beyond the caller's tensors.
 //
 // Two inner products are provided:
 //   * MFMA: the stage is an implicit GEMM  acc[m][p] += A[m][k] * B[k][p]
 //     with A = filter slice and B = the im2col view of the staged input
 //     (k = channel, filter row, filter column), fed to
-//     v_mfma_f32_32x32x2_f32.  Each MFMA consumes a channel pair (c, c+1) at
-//     one (r, s): lanes 0-31 supply channel c, lanes 32-63 channel c+1.
+//     v_mfma_f32_32x32x2_f32 (32 x 32 tiles; lanes 0-31 and 32-63 supply two
+//     channels c, c+1 at one (r, s)) or v_mfma_f32_16x16x4_f32 (16 x 16
+//     tiles; the four 16-lane groups supply channels c .. c+3).
 //   * VALU: one output pixel per lane and MR filters per wave, with the
 //     filter values wave-uniform in scalar registers and one fp32 FMA per
 //     term (packed fp32 FMAs are not used).
@@ -96,21 +96,16 @@ struct TileArgs {
   int tiles_x;        // output tiles along x
   int ntiles;         // output tiles per map
   int mtiles;         // filter tiles
-  int c_per_split;    // channels per workgroup along the channel sum
-  int split_c;        // workgroups along the channel sum
   int IH, IW, ICS;    // staged input tile rows, columns, channel stride
 };
 
-// Decompose the (remapped) linear block id into output tile, filter tile and
-// channel split.  Output tiles vary fastest so that workgroups sharing a
-// filter slice run close together.
-__device__ __forceinline__ void block_coords(const TileArgs &a, int &tile, int &mt, int &split) {
-  const int nblocks = a.ntiles * a.mtiles * a.split_c;
-  int b = xcd_remap(blockIdx.x, nblocks);
+// Decompose the (remapped) linear block id into output tile and filter tile.
+// Output tiles vary fastest, so workgroups sharing a filter slice run close
+// together (and, after the remap, on one XCD's L2).
+__device__ __forceinline__ void block_coords(const TileArgs &a, int &tile, int &mt) {
+  const int b = xcd_remap(blockIdx.x, a.ntiles * a.mtiles);
   tile = b % a.ntiles;
-  b /= a.ntiles;
-  mt = b % a.mtiles;
-  split = b / a.mtiles;
+  mt = b / a.ntiles;
 }
 
 // ---------------------------------------------------------------------------
@@ -134,52 +129,85 @@ __device__ __forceinline__ void dma_f32(const float *src, float *lds_row) {
 }
 
 constexpr int ceil_div(int a, int b) { return (a + b - 1) / b; }
+
+// The two fp32 matrix instructions.  MF x MF output tile per instruction,
+// KG lane groups each supplying one k value (lanes KG-group g = lane / MF,
+// row / column = lane % MF), NV accumulator registers per lane.
+template <int MF> struct Mfma;
+template <> struct Mfma<32> {
+  typedef float acc __attribute__((ext_vector_type(16)));
+  static constexpr int KG = 2, NV = 16;
+  static __device__ __forceinline__ acc mac(float a, float b, acc c) {
+    return __builtin_amdgcn_mfma_f32_32x32x2f32(a, b, c, 0, 0, 0);
+  }
+  // Row (filter within the 32) held by accumulator register v of `lane`;
+  // the column (pixel) is lane % 32.
+  static __device__ __forceinline__ int row(int lane, int v) {
+    return 8 * (v >> 2) + 4 * (lane >> 5) + (v & 3);
+  }
+};
+template <> struct Mfma<16> {
+  typedef float acc __attribute__((ext_vector_type(4)));
+  static constexpr int KG = 4, NV = 4;
+  static __device__ __forceinline__ acc mac(float a, float b, acc c) {
+    return __builtin_amdgcn_mfma_f32_16x16x4f32(a, b, c, 0, 0, 0);
+  }
+  // Row held by register v of `lane`; the column is lane % 16.
+  static __device__ __forceinline__ int row(int lane, int v) { return 4 * (lane >> 4) + v; }
+};
+
 // Staged geometry, in floats.
 //  * Filter rows: FROW = CC*K*K values per filter, copied in 64-lane chunks;
-//    row pitch FP = FROW rounded up to odd, so the 32 lanes that read one
-//    k-column of 32 filters hit 32 different banks.
+//    row pitch FP = FROW rounded up to odd, so the lanes that read one
+//    k-column of MF filters hit MF different banks.
 //  * Input planes: ICS floats per channel = the largest (tpy+K-1)*(tpx+K-1)
 //    over output tiles of at most PT pixels, K*(PT+K-1) (a 1 x PT or PT x 1
 //    tile), rounded up to whole 64-lane chunks so a plane is copied with
-//    unmasked chunks; planes of at most 32 floats (K = 1, 32-pixel tiles)
-//    take 32, and one 64-lane copy then fills two channels.
+//    unmasked chunks.  With 32x32 tiles, planes of at most 32 floats (K = 1,
+//    32-pixel tiles) take 32, and one 64-lane copy then fills two channels.
+//    With 16x16 tiles 16 floats are added, so that the lane groups reading
+//    neighbouring channels in one half-wave start 16 banks apart.
 constexpr int mfma_fp(int K, int CC) { return (CC * K * K) | 1; }
-constexpr int mfma_ics(int K, int PT) {
-  return K * (PT + K - 1) <= 32 ? 32 : 64 * ceil_div(K * (PT + K - 1), 64);
+constexpr int mfma_ics(int K, int PT, int MF) {
+  return MF == 32 && K * (PT + K - 1) <= 32 ? 32
+                                             : 64 * ceil_div(K * (PT + K - 1), 64) + (MF == 16 ? 16 : 0);
 }
 // Filter rows are copied by the NW waves in blocks of MT/NW consecutive
 // rows, each block followed by a 64-float gap (see the kernel's issue()).
 constexpr int mfma_fblk(int K, int MT, int CC, int NW) { return (MT / NW) * mfma_fp(K, CC) + 64; }
-constexpr int mfma_buf_floats(int K, int MT, int PT, int CC, int NW) {
-  return NW * mfma_fblk(K, MT, CC, NW) + CC * mfma_ics(K, PT);
+constexpr int mfma_buf_floats(int K, int MT, int PT, int CC, int NW, int MF) {
+  return NW * mfma_fblk(K, MT, CC, NW) + CC * mfma_ics(K, PT, MF);
 }
-// Channels per stage: the largest multiple of 2*WC (a channel pair per wave
-// group and k-step), at most 64, whose two stage buffers fit in 80 KB (two
-// four-wave workgroups per CU; an eight-wave workgroup fills a CU's SIMDs
-// with two waves each on its own, and longer stages measured no faster).
-//   A deep shape instead takes the largest power-of-two multiple of 2*WC, up
-// to 256 channels, whose two buffers fit in 160 KB (one workgroup per CU):
-// for small tiles with little work per channel (K = 1), where each stage
-// costs about one load latency whatever its size.
-constexpr int mfma_cc(int K, int MT, int PT, int WC, int NW, bool DEEP) {
-  int best = 2 * WC;
+// Channels per stage, a multiple of G = KG*WC (one k value per lane group of
+// every wave group and k-step): the largest such count, at most 64, whose
+// two stage buffers fit in 80 KB (two four-wave workgroups per CU; an
+// eight-wave workgroup fills a CU's SIMDs with two waves each on its own,
+// and longer stages measured no faster).
+//   A deep shape instead takes the largest power-of-two multiple of G, up to
+// 256 channels, whose two buffers fit in 160 KB (one workgroup per CU): for
+// small tiles with little work per channel (K = 1, small maps), where each
+// stage costs about one load latency whatever its size.
+constexpr int mfma_cc(int K, int MT, int PT, int G, int NW, bool DEEP, int MF) {
+  int best = G;
   if (DEEP) {
-    for (int cc = 2 * WC; cc <= 256; cc *= 2)
-      if (2 * mfma_buf_floats(K, MT, PT, cc, NW) * 4 <= 160 * 1024) best = cc;
+    for (int cc = G; cc <= 256; cc *= 2)
+      if (2 * mfma_buf_floats(K, MT, PT, cc, NW, MF) * 4 <= 160 * 1024) best = cc;
     return best;
   }
-  for (int cc = 2 * WC; cc <= 64; cc += 2 * WC)
-    if (2 * mfma_buf_floats(K, MT, PT, cc, NW) * 4 <= 80 * 1024) best = cc;
+  for (int cc = G; cc <= 64; cc += G)
+    if (2 * mfma_buf_floats(K, MT, PT, cc, NW, MF) * 4 <= 80 * 1024) best = cc;
   return best;
 }
 
-template <int K, int MB, int NB, int WM, int WN, int WC, bool DEEP>
+template <int K, int MF, int MB, int NB, int WM, int WN, int WC, bool DEEP>
 struct MfmaCfg {
   static constexpr int KK = K * K;
+  static constexpr int KG = Mfma<MF>::KG;
+  static constexpr int NV = Mfma<MF>::NV;
   static constexpr int NW = WM * WN * WC;   // waves per workgroup
-  static constexpr int MT = 32 * MB * WM;   // filters per workgroup
-  static constexpr int PT = 32 * NB * WN;   // pixel lanes per workgroup tile
-  static constexpr int CC = mfma_cc(K, MT, PT, WC, NW, DEEP);  // channels per stage
+  static constexpr int MT = MF * MB * WM;   // filters per workgroup
+  static constexpr int PT = MF * NB * WN;   // pixel lanes per workgroup tile
+  static constexpr int CC = mfma_cc(K, MT, PT, KG * WC, NW, DEEP, MF);  // channels per stage
   static constexpr int CCW = CC / WC;       // channels per wave group per stage
   static constexpr int FROW = CC * KK;      // staged floats per filter
   static constexpr int FP = mfma_fp(K, CC);
@@ -187,15 +215,16 @@ struct MfmaCfg {
   static constexpr int RPW = MT / NW;                  // filter rows copied per wave
   static constexpr int FBLK = mfma_fblk(K, MT, CC, NW);  // LDS stride of a wave's row block
   static constexpr int F_FLOATS = NW * FBLK;
-  static constexpr int ICS = mfma_ics(K, PT);
+  static constexpr int ICS = mfma_ics(K, PT, MF);
   static constexpr bool PAIR = ICS == 32;              // two input planes per 64-lane copy
   static constexpr int NCI = PAIR ? 1 : ICS / 64;      // most chunks an input plane needs
   static constexpr int BUF = F_FLOATS + CC * ICS;      // one stage buffer
-  static constexpr int RED = (WC - 1) * WM * WN * MB * NB * 1024;
+  static constexpr int ACC = NV * 64;                  // floats of one accumulator tile
+  static constexpr int RED = (WC - 1) * WM * WN * MB * NB * ACC;
   static constexpr int BUF0 = BUF > RED ? BUF : RED;   // buffer 0 also holds the WC sums
   static constexpr int LDS_BYTES = (BUF0 + BUF) * 4;
-  static_assert(NW == 4 || NW == 8, "four or eight waves per workgroup");
-  static_assert(CCW % 2 == 0, "channels are consumed in pairs");
+  static_assert(NW == 4 || NW == 8 || NW == 16, "four, eight or sixteen waves per workgroup");
+  static_assert(CCW % KG == 0, "each k-step takes one channel per lane group");
   static_assert(MT % NW == 0, "filter rows are shared out over the waves");
 };
 
@@ -206,27 +235,27 @@ struct MfmaCfg {
 // full stage is issued as unmasked 64-lane copies: lanes that fall outside
 // the map or past a filter row are pointed at valid elements whose values
 // only reach outputs that are never stored (or the padding of a row).
-template <int K, int MB, int NB, int WM, int WN, int WC, bool DEEP>
+template <int K, int MF, int MB, int NB, int WM, int WN, int WC, bool DEEP>
 __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__restrict__ I,
-                                                     const float *__restrict__ F,
-                                                     float *__restrict__ O,
-                                                     float *__restrict__ ws, TileArgs a) {
-  using Cfg = MfmaCfg<K, MB, NB, WM, WN, WC, DEEP>;
+                                                               const float *__restrict__ F,
+                                                               float *__restrict__ O, TileArgs a) {
+  using Cfg = MfmaCfg<K, MF, MB, NB, WM, WN, WC, DEEP>;
+  using Op = Mfma<MF>;
+  using acc_t = typename Op::acc;
   constexpr int KK = Cfg::KK, MT = Cfg::MT, CC = Cfg::CC, CCW = Cfg::CCW, FROW = Cfg::FROW;
   constexpr int FP = Cfg::FP, ICS = Cfg::ICS, F_FLOATS = Cfg::F_FLOATS;
   constexpr int NCF = Cfg::NCF, NCI = Cfg::NCI, RPW = Cfg::RPW, FBLK = Cfg::FBLK;
-  constexpr int NW = Cfg::NW, NTHR = 64 * NW;
+  constexpr int NW = Cfg::NW, NTHR = 64 * NW, KG = Cfg::KG, NV = Cfg::NV, ACC = Cfg::ACC;
   constexpr bool PAIR = Cfg::PAIR;
   __shared__ float buf0[Cfg::BUF0];
   __shared__ float buf1[Cfg::BUF];
 
-  int tile, mt, split;
-  block_coords(a, tile, mt, split);
+  int tile, mt;
+  block_coords(a, tile, mt);
   const int py0 = (tile / a.tiles_x) * a.tpy;
   const int px0 = (tile % a.tiles_x) * a.tpx;
   const int m0 = mt * MT;
-  const int c_begin = split * a.c_per_split;
-  const int c_end = min(a.C, c_begin + a.c_per_split);
+  const int c_end = a.C;
   const int Hout = a.Wy - K + 1;
   const int Wout = a.Wx - K + 1;
 
@@ -236,29 +265,29 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   const int wmn = wave / WC;
   const int wm = wmn % WM;
   const int wn = wmn / WM;
-  const int col = lane & 31;
-  const int half = lane >> 5;
+  const int col = lane % MF;   // filter row of A / pixel of B this lane supplies
+  const int grp = lane / MF;   // which of the KG channels of a k-step
 
   int a_base[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
-    const int row = wm * 32 * MB + mb * 32 + col;
-    a_base[mb] = (row / RPW) * FBLK + (row % RPW) * FP + (wc * CCW + half) * KK;
+    const int row = wm * MF * MB + mb * MF + col;
+    a_base[mb] = (row / RPW) * FBLK + (row % RPW) * FP + (wc * CCW + grp) * KK;
   }
   int b_base[NB];
   const int npix = a.tpy * a.tpx;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int p = wn * 32 * NB + nb * 32 + col;
+    const int p = wn * MF * NB + nb * MF + col;
     int off = 0;  // padding lanes read pixel (0, 0); their results are dropped
     if (p < npix) {
       const int ty = p / a.tpx;
       off = ty * a.IW + (p - ty * a.tpx);
     }
-    b_base[nb] = F_FLOATS + (wc * CCW + half) * ICS + off;
+    b_base[nb] = F_FLOATS + (wc * CCW + grp) * ICS + off;
   }
   // One input address per filter row r: every B read of a stage is then
-  // b_row[nb][r] plus a compile-time offset (channel pair and column).
+  // b_row[nb][r] plus a compile-time offset (channel group and column).
   int b_row[NB][K];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb)
@@ -302,13 +331,13 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   const int ofs_last = f_spill ? (int)frow_stride + e_next : e_last;
   const int ofs_last_end = f_spill ? 0 : e_last;
 
-  floatx16 acc[MB][NB];
+  acc_t acc[MB][NB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
     for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) acc[mb][nb][v] = 0.f;
+      for (int v = 0; v < NV; ++v) acc[mb][nb][v] = 0.f;
 
   // Start the loads of the stage at channel c0 into `buf`: filter row r to
   // buf[(r / RPW)*FBLK + (r % RPW)*FP + e], input planes to
@@ -407,12 +436,12 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     }
   };
 
-  // The stage's k-steps (channel pair cp, filter row r, filter column s) run
+  // The stage's k-steps (channel group cg, filter row r, filter column s) run
   // in chunks of L with one chunk of operand look-ahead from LDS.  The empty
   // asm statements on the accumulators and the scheduling barriers keep the
   // compiler from hoisting every LDS read of the stage into registers.
   auto compute = [&](const float *buf) {
-    constexpr int NQ = (CCW / 2) * KK;
+    constexpr int NQ = (CCW / KG) * KK;
     constexpr int L = 4;
     constexpr int NCH = (NQ + L - 1) / L;
     float ca[L][MB], cb[L][NB], na[L][MB], nbv[L][NB];
@@ -421,11 +450,11 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
       for (int l = 0; l < L; ++l) {
         const int q = ch * L + l;
         if (q < NQ) {
-          const int cp = q / KK, r = (q % KK) / K, s = q % K;
+          const int cg = q / KK, r = (q % KK) / K, s = q % K;
 #pragma unroll
-          for (int mb = 0; mb < MB; ++mb) av[l][mb] = buf[a_base[mb] + 2 * cp * KK + r * K + s];
+          for (int mb = 0; mb < MB; ++mb) av[l][mb] = buf[a_base[mb] + KG * cg * KK + r * K + s];
 #pragma unroll
-          for (int nb = 0; nb < NB; ++nb) bv[l][nb] = buf[b_row[nb][r] + 2 * cp * ICS + s];
+          for (int nb = 0; nb < NB; ++nb) bv[l][nb] = buf[b_row[nb][r] + KG * cg * ICS + s];
         }
       }
     };
@@ -447,9 +476,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 #pragma unroll
           for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-            for (int nb = 0; nb < NB; ++nb)
-              acc[mb][nb] =
-                  __builtin_amdgcn_mfma_f32_32x32x2f32(ca[l][mb], cb[l][nb], acc[mb][nb], 0, 0, 0);
+            for (int nb = 0; nb < NB; ++nb) acc[mb][nb] = Op::mac(ca[l][mb], cb[l][nb], acc[mb][nb]);
         }
       }
 #pragma unroll
@@ -467,8 +494,8 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     }
   };
 
-  issue(c_begin, buf0);
-  for (int c0 = c_begin; c0 < c_end; c0 += 2 * CC) {
+  issue(0, buf0);
+  for (int c0 = 0; c0 < c_end; c0 += 2 * CC) {
     wait_lds_dma();
     lds_barrier();  // stage c0 is in buf0; buf1 is free
     if (c0 + CC < c_end) issue(c0 + CC, buf1);
@@ -480,7 +507,8 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     compute(buf1);
   }
 
-  // Fixed-order sum of the WC channel groups through LDS.
+  // Fixed-order sum of the WC channel groups through LDS: group 0 adds the
+  // partial tiles of groups 1, 2, ..., WC-1 in that order.
   if constexpr (WC > 1) {
     float *red = buf0;
     lds_barrier();  // every wave is done with the stage buffers
@@ -490,8 +518,8 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-          for (int v = 0; v < 16; ++v)
-            red[((((wc - 1) * WM * WN + wmn) * MB + mb) * NB + nb) * 1024 + v * 64 + lane] =
+          for (int v = 0; v < NV; ++v)
+            red[((((wc - 1) * WM * WN + wmn) * MB + mb) * NB + nb) * ACC + v * 64 + lane] =
                 acc[mb][nb][v];
     }
     lds_barrier();
@@ -503,14 +531,13 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-          for (int v = 0; v < 16; ++v)
-            acc[mb][nb][v] += red[((((g - 1) * WM * WN + wmn) * MB + mb) * NB + nb) * 1024 + v * 64 + lane];
+          for (int v = 0; v < NV; ++v)
+            acc[mb][nb][v] += red[((((g - 1) * WM * WN + wmn) * MB + mb) * NB + nb) * ACC + v * 64 + lane];
   }
 
-  float *dst = (a.split_c == 1) ? O : ws + (size_t)split * a.M * Hout * Wout;
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
-    const int p = wn * 32 * NB + nb * 32 + col;
+    const int p = wn * MF * NB + nb * MF + col;
     if (p >= npix) continue;
     const int ty = p / a.tpx;
     const int gy = py0 + ty;
@@ -520,10 +547,9 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 #pragma unroll
     for (int mb = 0; mb < MB; ++mb)
 #pragma unroll
-      for (int v = 0; v < 16; ++v) {
-        const int i = 8 * (v >> 2) + 4 * half + (v & 3);
-        const int m = m0 + wm * 32 * MB + mb * 32 + i;
-        if (m < a.M) dst[(size_t)m * Hout * Wout + pix] = acc[mb][nb][v];
+      for (int v = 0; v < NV; ++v) {
+        const int m = m0 + wm * MF * MB + mb * MF + Op::row(lane, v);
+        if (m < a.M) O[(size_t)m * Hout * Wout + pix] = acc[mb][nb][v];
       }
   }
 }
@@ -535,8 +561,8 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 template <int KT, int MR, int WC, int CC>
 __global__ __launch_bounds__(kBlock) void multi_valu(const float *__restrict__ I,
                                                      const float *__restrict__ F,
-                                                     float *__restrict__ O,
-                                                     float *__restrict__ ws, TileArgs a, int Krt) {
+                                                     float *__restrict__ O, TileArgs a,
+                                                     int Krt) {
   constexpr int CCW = CC / WC;
   constexpr int WMV = 4 / WC;     // filter groups per workgroup
   constexpr int MT = MR * WMV;
@@ -545,12 +571,11 @@ __global__ __launch_bounds__(kBlock) void multi_valu(const float *__restrict__ I
   extern __shared__ float lds[];
   float *Is = lds;
 
-  int tile, mt, split;
-  block_coords(a, tile, mt, split);
+  int tile, mt;
+  block_coords(a, tile, mt);
   const int py0 = (tile / a.tiles_x) * a.tpy;
   const int px0 = (tile % a.tiles_x) * a.tpx;
-  const int c_begin = split * a.c_per_split;
-  const int c_end = min(a.C, c_begin + a.c_per_split);
+  const int c_end = a.C;
   const int Hout = a.Wy - K + 1;
   const int Wout = a.Wx - K + 1;
 
@@ -577,7 +602,7 @@ __global__ __launch_bounds__(kBlock) void multi_valu(const float *__restrict__ I
 #pragma unroll
   for (int mr = 0; mr < MR; ++mr) acc[mr] = 0.f;
 
-  for (int c0 = c_begin; c0 < c_end; c0 += CC) {
+  for (int c0 = 0; c0 < c_end; c0 += CC) {
     stage_input(Is, I, CC, c0, c_end, py0, px0, a.IH, a.IW, a.ICS, a.Wx, a.Wy);
     __syncthreads();
     for (int cl = wc * CCW; cl < (wc + 1) * CCW; ++cl) {
@@ -630,11 +655,10 @@ __global__ __launch_bounds__(kBlock) void multi_valu(const float *__restrict__ I
   const int gy = py0 + ty;
   const int gx = px0 + (lane - ty * a.tpx);
   if (gy >= Hout || gx >= Wout) return;
-  float *dst = (a.split_c == 1) ? O : ws + (size_t)split * a.M * Hout * Wout;
   const size_t pix = (size_t)gy * Wout + gx;
 #pragma unroll
   for (int mr = 0; mr < MR; ++mr)
-    if (mbase + mr < a.M) dst[(size_t)(mbase + mr) * Hout * Wout + pix] = acc[mr];
+    if (mbase + mr < a.M) O[(size_t)(mbase + mr) * Hout * Wout + pix] = acc[mr];
 }
 
 // Any size: one output per thread, operands read through the caches.  Used
@@ -663,31 +687,6 @@ __global__ __launch_bounds__(256) void multi_generic(const float *__restrict__ I
   O[idx] = acc;
 }
 
-// O[i] = sum_{s < S} ws[s][i], added in the order s = 0, 1, ..., S-1.  Each
-// thread sums V consecutive outputs (V = 4: 16-byte loads and stores) and
-// issues the loads of up to 16 slots before adding them, so one memory
-// latency covers the common split factors.
-template <int V>
-__global__ __launch_bounds__(256) void split_sum(const float *__restrict__ ws,
-                                                 float *__restrict__ O, int64_t n, int S) {
-  typedef float vec __attribute__((ext_vector_type(V)));
-  const int64_t nv = n / V;
-  const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
-  if (i >= nv) return;
-  const vec *src = reinterpret_cast<const vec *>(ws) + i;
-  vec acc = src[0];
-  for (int s0 = 1; s0 < S; s0 += 16) {
-    vec v[16];
-#pragma unroll
-    for (int j = 0; j < 16; ++j)
-      if (s0 + j < S) v[j] = src[(int64_t)(s0 + j) * nv];
-#pragma unroll
-    for (int j = 0; j < 16; ++j)
-      if (s0 + j < S) acc += v[j];
-  }
-  reinterpret_cast<vec *>(O)[i] = acc;
-}
-
 // Dynamic LDS per workgroup the planner may request (gfx950: 160 KB per CU).
 constexpr int kMaxLds = 160 * 1024;
 
@@ -704,17 +703,24 @@ hipError_t allow_full_lds(Kern kern) {
 // Kernel table
 // ---------------------------------------------------------------------------
 // Each family has a few workgroup shapes; the planner picks one per call.
-struct MfmaShape { int MB, NB, WM, WN, WC; bool deep; };
+// MF: 32 (v_mfma_f32_32x32x2_f32) or 16 (v_mfma_f32_16x16x4_f32) tiles.
+struct MfmaShape { int MF, MB, NB, WM, WN, WC; bool deep; };
 constexpr MfmaShape kMfmaShapes[] = {
-    {1, 1, 2, 1, 2, false},  // 64 filters x 32 pixels, channel sum split over 2 wave pairs
-    {1, 2, 1, 2, 2, false},  // 32 x 128, channel sum split over 2 wave pairs
-    {1, 1, 2, 2, 1, false},  // 64 x 64
-    {1, 2, 2, 2, 1, false},  // 64 x 128
-    {2, 2, 2, 2, 1, false},  // 128 x 128
-    {1, 2, 1, 1, 4, false},  // 32 x 64, channel sum split over 4 waves
-    {1, 1, 2, 2, 2, false},  // 64 x 64, eight waves, channel sum split over 2 wave groups
-    {1, 1, 2, 4, 1, false},  // 64 x 128, eight waves
-    {1, 1, 1, 1, 4, true},   // 32 x 32, channel sum split over 4 waves, deep stages
+    {32, 1, 1, 2, 1, 2, false},  // 64 filters x 32 pixels, channel sum split over 2 wave pairs
+    {32, 1, 2, 1, 2, 2, false},  // 32 x 128, channel sum split over 2 wave pairs
+    {32, 1, 1, 2, 2, 1, false},  // 64 x 64
+    {32, 1, 2, 2, 2, 1, false},  // 64 x 128
+    {32, 2, 2, 2, 2, 1, false},  // 128 x 128
+    {32, 1, 2, 1, 1, 4, false},  // 32 x 64, channel sum split over 4 waves
+    {32, 1, 1, 2, 2, 2, false},  // 64 x 64, eight waves, channel sum split over 2 wave groups
+    {32, 1, 1, 2, 4, 1, false},  // 64 x 128, eight waves
+    {32, 1, 1, 1, 1, 4, true},   // 32 x 32, channel sum split over 4 waves, deep stages
+    {32, 1, 1, 1, 1, 8, true},   // 32 x 32, eight waves splitting the channel sum, deep stages
+    {16, 1, 1, 1, 1, 16, true},  // 16 x 16, sixteen waves splitting the channel sum, deep stages
+    {16, 1, 1, 1, 1, 8, false},  // 16 x 16, eight waves splitting the channel sum
+    {16, 1, 1, 1, 1, 4, false},  // 16 x 16, four waves splitting the channel sum
+    {16, 1, 1, 2, 1, 4, false},  // 32 x 16, eight waves (four per 16 filters)
+    {16, 1, 1, 1, 2, 4, false},  // 16 x 32, eight waves (four per 16 pixels)
 };
 constexpr int kNumMfma = sizeof(kMfmaShapes) / sizeof(kMfmaShapes[0]);
 
@@ -726,54 +732,55 @@ constexpr ValuShape kValuShapes[] = {
 constexpr int kNumValu = sizeof(kValuShapes) / sizeof(kValuShapes[0]);
 
 template <int K, int S>
+using ShapeCfg = MfmaCfg<K, kMfmaShapes[S].MF, kMfmaShapes[S].MB, kMfmaShapes[S].NB,
+                         kMfmaShapes[S].WM, kMfmaShapes[S].WN, kMfmaShapes[S].WC,
+                         kMfmaShapes[S].deep>;
+
+template <int K, int S>
 hipError_t launch_mfma_shape(const MultiPlan &p, const float *I, const float *F, float *O,
-                             float *ws, const TileArgs &a, hipStream_t st) {
+                             const TileArgs &a, hipStream_t st) {
   constexpr MfmaShape sh = kMfmaShapes[S];
   // Shapes whose stage buffers exceed the LDS for this K are never planned
   // (the candidate list drops them) and are not instantiated.
-  if constexpr (MfmaCfg<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC, sh.deep>::LDS_BYTES > kMaxLds) {
+  if constexpr (ShapeCfg<K, S>::LDS_BYTES > kMaxLds) {
     return hipErrorInvalidValue;
   } else {
-    auto kern = multi_mfma<K, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC, sh.deep>;
-    hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(64 * sh.WM * sh.WN * sh.WC), 0, st, I, F, O, ws,
-                       a);
+    auto kern = multi_mfma<K, sh.MF, sh.MB, sh.NB, sh.WM, sh.WN, sh.WC, sh.deep>;
+    hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(64 * sh.WM * sh.WN * sh.WC), 0, st, I, F, O, a);
     return hipGetLastError();
   }
 }
 
+template <int K, int... S>
+hipError_t launch_mfma_k(const MultiPlan &p, const float *I, const float *F, float *O,
+                         const TileArgs &a, hipStream_t st, std::integer_sequence<int, S...>) {
+  hipError_t e = hipErrorInvalidValue;
+  ((p.kernel == S ? (e = launch_mfma_shape<K, S>(p, I, F, O, a, st), 0) : 0), ...);
+  return e;
+}
+
 template <int K>
 hipError_t launch_mfma_k(const MultiPlan &p, const float *I, const float *F, float *O,
-                         float *ws, const TileArgs &a, hipStream_t st) {
-  switch (p.kernel) {
-    case 0: return launch_mfma_shape<K, 0>(p, I, F, O, ws, a, st);
-    case 1: return launch_mfma_shape<K, 1>(p, I, F, O, ws, a, st);
-    case 2: return launch_mfma_shape<K, 2>(p, I, F, O, ws, a, st);
-    case 3: return launch_mfma_shape<K, 3>(p, I, F, O, ws, a, st);
-    case 4: return launch_mfma_shape<K, 4>(p, I, F, O, ws, a, st);
-    case 5: return launch_mfma_shape<K, 5>(p, I, F, O, ws, a, st);
-    case 6: return launch_mfma_shape<K, 6>(p, I, F, O, ws, a, st);
-    case 7: return launch_mfma_shape<K, 7>(p, I, F, O, ws, a, st);
-    case 8: return launch_mfma_shape<K, 8>(p, I, F, O, ws, a, st);
-    default: return hipErrorInvalidValue;
-  }
+                         const TileArgs &a, hipStream_t st) {
+  return launch_mfma_k<K>(p, I, F, O, a, st, std::make_integer_sequence<int, kNumMfma>{});
 }
 
 template <int KT, int S>
 hipError_t launch_valu_shape(const MultiPlan &p, const float *I, const float *F, float *O,
-                             float *ws, const TileArgs &a, hipStream_t st) {
+                             const TileArgs &a, hipStream_t st) {
   constexpr ValuShape sh = kValuShapes[S];
   auto kern = multi_valu<KT, sh.MR, sh.WC, sh.CC>;
   if (hipError_t e = allow_full_lds(kern); e != hipSuccess) return e;
-  hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(kBlock), p.lds_bytes, st, I, F, O, ws, a, p.K);
+  hipLaunchKernelGGL(kern, dim3(p.grid_x), dim3(kBlock), p.lds_bytes, st, I, F, O, a, p.K);
   return hipGetLastError();
 }
 
 template <int KT>
 hipError_t launch_valu_k(const MultiPlan &p, const float *I, const float *F, float *O,
-                         float *ws, const TileArgs &a, hipStream_t st) {
+                         const TileArgs &a, hipStream_t st) {
   switch (p.kernel) {
-    case 0: return launch_valu_shape<KT, 0>(p, I, F, O, ws, a, st);
-    case 1: return launch_valu_shape<KT, 1>(p, I, F, O, ws, a, st);
+    case 0: return launch_valu_shape<KT, 0>(p, I, F, O, a, st);
+    case 1: return launch_valu_shape<KT, 1>(p, I, F, O, a, st);
     default: return hipErrorInvalidValue;
   }
 }
@@ -806,86 +813,124 @@ TileChoice choose_tile(int Hout, int Wout, int cap) {
 
 struct Candidate {
   int kernel, MT, PT, WC, CC;
-  int ops_per_kstep;  // MFMAs per wave per (channel pair, r, s); VALU: FMAs per lane per (c, r, s)
+  int mf;             // MFMA tile (32 or 16); 0 for the vector family
+  int ops_per_kstep;  // MFMAs per wave per k-step; VALU: FMAs per lane per (c, r, s)
   int lds_fixed;      // static LDS bytes (MFMA family), 0 if it depends on the tile
   int red_floats;     // LDS floats for the in-workgroup channel-group sum
   int waves;          // waves per workgroup
 };
 
+template <int S>
+int shape_lds_bytes(int K) {
+  switch (K) {
+    case 1: return ShapeCfg<1, S>::LDS_BYTES;
+    case 2: return ShapeCfg<2, S>::LDS_BYTES;
+    case 3: return ShapeCfg<3, S>::LDS_BYTES;
+    case 4: return ShapeCfg<4, S>::LDS_BYTES;
+    case 5: return ShapeCfg<5, S>::LDS_BYTES;
+    case 6: return ShapeCfg<6, S>::LDS_BYTES;
+    case 7: return ShapeCfg<7, S>::LDS_BYTES;
+    default: return INT32_MAX;
+  }
+}
+
+template <int S>
+int shape_cc(int K) {
+  switch (K) {
+    case 1: return ShapeCfg<1, S>::CC;
+    case 2: return ShapeCfg<2, S>::CC;
+    case 3: return ShapeCfg<3, S>::CC;
+    case 4: return ShapeCfg<4, S>::CC;
+    case 5: return ShapeCfg<5, S>::CC;
+    case 6: return ShapeCfg<6, S>::CC;
+    case 7: return ShapeCfg<7, S>::CC;
+    default: return 0;
+  }
+}
+
+// The compile-time configuration of shape i at filter size K (the kernels'
+// own constants, so the planner and the kernels cannot disagree).
+template <int... S>
+void shape_consts(int i, int K, int &cc, int &lds, std::integer_sequence<int, S...>) {
+  ((i == S ? (cc = shape_cc<S>(K), lds = shape_lds_bytes<S>(K), 0) : 0), ...);
+}
+
 Candidate mfma_candidate(int i, int K) {
   const MfmaShape s = kMfmaShapes[i];
-  const int MT = 32 * s.MB * s.WM, PT = 32 * s.NB * s.WN;
+  const int MT = s.MF * s.MB * s.WM, PT = s.MF * s.NB * s.WN;
   const int NW = s.WM * s.WN * s.WC;
-  const int CC = mfma_cc(K, MT, PT, s.WC, NW, s.deep);
-  const int buf = mfma_buf_floats(K, MT, PT, CC, NW);
-  const int red = (s.WC - 1) * s.WM * s.WN * s.MB * s.NB * 1024;
-  return Candidate{i, MT, PT, s.WC, CC, s.MB * s.NB, ((buf > red ? buf : red) + buf) * 4, red, NW};
+  int cc = 0, lds = 0;
+  shape_consts(i, K, cc, lds, std::make_integer_sequence<int, kNumMfma>{});
+  const int red = (s.WC - 1) * s.WM * s.WN * s.MB * s.NB * s.MF * s.MF;
+  return Candidate{i, MT, PT, s.WC, cc, s.MF, s.MB * s.NB, lds, red, NW};
 }
 
 Candidate valu_candidate(int i) {
   const ValuShape s = kValuShapes[i];
-  return Candidate{i, s.MR * (4 / s.WC), 64, s.WC, s.CC, s.MR, 0, (s.WC - 1) * (4 / s.WC) * s.MR * 64,
-                   4};
+  return Candidate{i, s.MR * (4 / s.WC), 64, s.WC, s.CC, 0, s.MR,
+                   0, (s.WC - 1) * (4 / s.WC) * s.MR * 64, 4};
 }
 
 // Rough time model in GPU clock cycles, used only to rank candidates.
 //   work:  inner-product plus per-stage bookkeeping cycles of the busiest CU
 //          (co-resident workgroups share its four SIMDs; a SIMD with a
 //          single wave issues its MFMAs less densely than one with two);
-//          splitting the stage's channels over WC wave groups adds their LDS
-//          reduction
+//          splitting the channels over WC wave groups adds their LDS
+//          reduction at the end
 //   chain: a workgroup's stages cannot run faster than the load latency
 //          (the MFMA family overlaps the next stage's loads with the current
 //          stage; the VALU family pays the latency every stage); `occ`
 //          co-resident workgroups overlap each other's chains
-//   split: partial sums written, re-read and added by a second launch
+//   copy:  the bytes a CU stages into LDS, at the rate one CU's vector
+//          memory path delivers them
 // The constants were fitted to exhaustive timings of every candidate plan of
-// nineteen layer shapes on an MI355X (the fitted model picks a plan within
-// about 1% of the fastest on average, 7% at worst).
-double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int Hout, int Wout,
-                int num_cu, const TileChoice &t, int split, int cps, int64_t lds_bytes) {
+// the layer shapes in the benchmark set on an MI355X.
+double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
+                const TileChoice &t, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
   const int64_t mtiles = (M + cd.MT - 1) / cd.MT;
-  const int64_t blocks = ntiles * mtiles * split;
-  const int stages = (cps + cd.CC - 1) / cd.CC;
+  const int64_t blocks = ntiles * mtiles;
+  const int stages = (C + cd.CC - 1) / cd.CC;
   const int kk = K * K;
   // Fitted per family: the matrix-core kernels on every layer with their
   // eight-wave and deep shapes, the vector kernels on the same layers.
-  constexpr double kMfmaCycles = 80.0;    // one 32x32x2 MFMA per wave (issue: 64)
+  constexpr double kMfma32Cycles = 80.0;  // one 32x32x2 MFMA per wave (issue: 64)
+  constexpr double kMfma16Cycles = 40.0;  // one 16x16x4 MFMA per wave (issue: 32)
   constexpr double kOneWavePerSimd = 1.3; // MFMA cycles factor with one wave per SIMD
-  constexpr double kWcReduction = 500.0;  // per extra wave group, per stage
+  constexpr double kWcReduction = 300.0;  // per extra wave group
   constexpr double kLaunch = 2000.0;
+  constexpr double kCopyBytesPerClock = 48.0;
   const double kStageOverhead = mfma ? 1200.0 : 300.0;
   const double kLatency = mfma ? 5000.0 : 2000.0;
-  const double kSplitLaunch = mfma ? 5000.0 : 2000.0;
-  const double kSplitBytesPerClock = mfma ? 1000.0 : 2000.0;
-  constexpr int kMaxOcc = 2;              // four-wave workgroups per CU
+  constexpr int kMaxWaves = 8;            // co-resident waves per CU the model counts
   int occ = (int)(160 * 1024 / (lds_bytes > 0 ? lds_bytes : 1));
-  if (occ > kMaxOcc * 4 / cd.waves) occ = kMaxOcc * 4 / cd.waves;
+  if (occ > kMaxWaves / cd.waves) occ = kMaxWaves / cd.waves;
   if (occ < 1) occ = 1;
   const int64_t per_cu = (blocks + num_cu - 1) / num_cu;
   const int64_t rounds = (per_cu + occ - 1) / occ;
   const int64_t waves_per_simd = cd.waves / 4 * (per_cu < occ ? per_cu : occ);
-  // (eight-wave workgroups put two waves on each SIMD)
+  const int kg = cd.mf == 16 ? 4 : 2;
+  const double mcyc = cd.mf == 16 ? kMfma16Cycles : kMfma32Cycles;
   const double per_stage =
-      (mfma ? (double)(cd.CC / cd.WC / 2) * kk * cd.ops_per_kstep * kMfmaCycles * cd.waves / 4 *
+      (mfma ? (double)(cd.CC / cd.WC / kg) * kk * cd.ops_per_kstep * mcyc * cd.waves / 4 *
                   (waves_per_simd < 2 ? kOneWavePerSimd : 1.0)
             : (double)(cd.CC / cd.WC) * kk * cd.ops_per_kstep * 4.0) +
-      kStageOverhead + (cd.WC - 1) * kWcReduction;
+      kStageOverhead;
   const double work = (double)per_cu * stages * per_stage;
   const double stage_chain = mfma ? (per_stage > kLatency ? per_stage : kLatency)
                                   : per_stage + kLatency;
   const double chain = (double)rounds * stages * stage_chain;
-  double extra = 0.0;
-  if (split > 1) {
-    const double bytes = 2.0 * split * (double)M * Hout * Wout * 4.0;
-    extra = kSplitLaunch + bytes / kSplitBytesPerClock;
-  }
-  return (work > chain ? work : chain) + kLatency + kLaunch + extra;
+  // Bytes staged per workgroup: the filter slice and the input halo tile of
+  // every channel.
+  const double staged = 4.0 * C * ((double)cd.MT * kk + (t.tpy + K - 1.0) * (t.tpx + K - 1.0));
+  const double copy = mfma ? (double)per_cu * staged / kCopyBytesPerClock : 0.0;
+  double tm = work > chain ? work : chain;
+  if (copy > tm) tm = copy;
+  return tm + (cd.WC - 1) * kWcReduction + kLatency + kLaunch;
 }
 
-// Every (shape, channel split) of one family whose LDS footprint fits, with
-// the time model's estimate, in a fixed order (shape, then split).
+// Every workgroup shape of one family whose LDS footprint fits, with the
+// time model's estimate, in a fixed order.
 void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu,
                       std::vector<std::pair<double, MultiPlan>> &out) {
   const int Hout = Wy - K + 1, Wout = Wx - K + 1;
@@ -900,33 +945,24 @@ void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu
       lds_bytes = 4 * (stage > cd.red_floats ? stage : cd.red_floats);
     }
     if (lds_bytes > kMaxLds) continue;
-    for (int split = 1; split <= 64; split *= 2) {
-      // channels per split: a multiple of the stage size
-      int cps = (C + split - 1) / split;
-      cps = (cps + cd.CC - 1) / cd.CC * cd.CC;
-      const int real_split = (C + cps - 1) / cps;
-      if (real_split != split) break;
-      const double tm = estimate(cd, mfma, C, M, K, Hout, Wout, num_cu, t, split, cps, lds_bytes);
-      MultiPlan p{};
-      p.variant = mfma ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
-      p.kernel = i;
-      p.K = K;
-      p.tile_m = cd.MT;
-      p.tpy = t.tpy;
-      p.tpx = t.tpx;
-      p.tiles_x = t.tiles_x;
-      p.tiles_y = t.tiles_y;
-      p.chunk_c = cd.CC;
-      p.split_c = split;
-      p.c_per_split = cps;
-      p.grid_x = (int)((int64_t)t.tiles_x * t.tiles_y * ((M + cd.MT - 1) / cd.MT) * split);
-      p.grid_y = 1;
-      p.grid_z = 1;
-      p.block = 64 * cd.waves;
-      p.lds_bytes = (int)lds_bytes;
-      p.workspace_bytes = split > 1 ? (int64_t)split * M * Hout * Wout * 4 : 0;
-      out.emplace_back(tm, p);
-    }
+    const double tm = estimate(cd, mfma, C, M, K, num_cu, t, lds_bytes);
+    MultiPlan p{};
+    p.variant = mfma ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
+    p.kernel = i;
+    p.K = K;
+    p.tile_m = cd.MT;
+    p.tpy = t.tpy;
+    p.tpx = t.tpx;
+    p.tiles_x = t.tiles_x;
+    p.tiles_y = t.tiles_y;
+    p.chunk_c = cd.CC;
+    p.waves_c = cd.WC;
+    p.grid_x = (int)((int64_t)t.tiles_x * t.tiles_y * ((M + cd.MT - 1) / cd.MT));
+    p.grid_y = 1;
+    p.grid_z = 1;
+    p.block = 64 * cd.waves;
+    p.lds_bytes = (int)lds_bytes;
+    out.emplace_back(tm, p);
   }
   if (out.empty() && !mfma) {
     // No tiled shape fits in LDS: one output per thread from the caches.
@@ -941,13 +977,11 @@ void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu
     p.tiles_x = Wout;
     p.tiles_y = Hout;
     p.chunk_c = C;
-    p.split_c = 1;
-    p.c_per_split = C;
+    p.waves_c = 1;
     p.grid_x = (int)((total + 255) / 256);
     p.grid_y = p.grid_z = 1;
     p.block = 256;
     p.lds_bytes = 0;
-    p.workspace_bytes = 0;
     out.emplace_back(0.0, p);
   }
 }
@@ -986,13 +1020,12 @@ void export_multi_plan(const MultiPlan &p, dconv_plan *out) {
   out->tile_h = p.tpy;
   out->tile_w = p.tpx;
   out->chunk_c = p.chunk_c;
-  out->split_c = p.split_c;
+  out->waves_c = p.waves_c;
   out->grid_x = p.grid_x;
   out->grid_y = p.grid_y;
   out->grid_z = p.grid_z;
   out->block = p.block;
   out->lds_bytes = p.lds_bytes;
-  out->workspace_bytes = p.workspace_bytes;
 }
 
 int multi_candidates(int C, int M, int Wx, int Wy, int K, int variant, int num_cu,
@@ -1008,8 +1041,8 @@ int multi_candidates(int C, int M, int Wx, int Wy, int K, int variant, int num_c
   return out.empty() ? DCONV_EUNSUPPORTED : DCONV_OK;
 }
 
-hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, float *O, float *ws,
-                        int C, int M, int Wx, int Wy, hipStream_t st) {
+hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, float *O, int C,
+                        int M, int Wx, int Wy, hipStream_t st) {
   TileArgs a{};
   a.C = C;
   a.M = M;
@@ -1020,50 +1053,35 @@ hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, floa
   a.tiles_x = p.tiles_x;
   a.ntiles = p.tiles_x * p.tiles_y;
   a.mtiles = (M + p.tile_m - 1) / p.tile_m;
-  a.c_per_split = p.c_per_split;
-  a.split_c = p.split_c;
   a.IH = p.tpy + p.K - 1;
   a.IW = p.tpx + p.K - 1;
   a.ICS = a.IH * a.IW;
-  hipError_t e;
   if (p.kernel == kGenericKernel) {
     hipLaunchKernelGGL(multi_generic, dim3(p.grid_x), dim3(256), 0, st, I, F, O, C, M, Wx, Wy, p.K);
     return hipGetLastError();
   }
   if (p.variant == DCONV_VARIANT_MFMA) {
     switch (p.K) {
-      case 1: e = launch_mfma_k<1>(p, I, F, O, ws, a, st); break;
-      case 2: e = launch_mfma_k<2>(p, I, F, O, ws, a, st); break;
-      case 3: e = launch_mfma_k<3>(p, I, F, O, ws, a, st); break;
-      case 4: e = launch_mfma_k<4>(p, I, F, O, ws, a, st); break;
-      case 5: e = launch_mfma_k<5>(p, I, F, O, ws, a, st); break;
-      case 6: e = launch_mfma_k<6>(p, I, F, O, ws, a, st); break;
-      case 7: e = launch_mfma_k<7>(p, I, F, O, ws, a, st); break;
+      case 1: return launch_mfma_k<1>(p, I, F, O, a, st);
+      case 2: return launch_mfma_k<2>(p, I, F, O, a, st);
+      case 3: return launch_mfma_k<3>(p, I, F, O, a, st);
+      case 4: return launch_mfma_k<4>(p, I, F, O, a, st);
+      case 5: return launch_mfma_k<5>(p, I, F, O, a, st);
+      case 6: return launch_mfma_k<6>(p, I, F, O, a, st);
+      case 7: return launch_mfma_k<7>(p, I, F, O, a, st);
       default: return hipErrorInvalidValue;
     }
-  } else {
-    switch (p.K) {
-      case 1: e = launch_valu_k<1>(p, I, F, O, ws, a, st); break;
-      case 2: e = launch_valu_k<2>(p, I, F, O, ws, a, st); break;
-      case 3: e = launch_valu_k<3>(p, I, F, O, ws, a, st); break;
-      case 4: e = launch_valu_k<4>(p, I, F, O, ws, a, st); break;
-      case 5: e = launch_valu_k<5>(p, I, F, O, ws, a, st); break;
-      case 6: e = launch_valu_k<6>(p, I, F, O, ws, a, st); break;
-      case 7: e = launch_valu_k<7>(p, I, F, O, ws, a, st); break;
-      default: e = launch_valu_k<0>(p, I, F, O, ws, a, st); break;
-    }
   }
-  if (e != hipSuccess || p.split_c == 1) return e;
-  const int64_t n = (int64_t)M * (Wy - p.K + 1) * (Wx - p.K + 1);
-  // The workspace comes from the device allocator (256-byte aligned); with
-  // n % 4 == 0 every slot starts on a 16-byte boundary.
-  if (n % 4 == 0 && (reinterpret_cast<uintptr_t>(O) & 15) == 0)
-    hipLaunchKernelGGL(split_sum<4>, dim3((unsigned)((n / 4 + 255) / 256)), dim3(256), 0, st, ws,
-                       O, n, p.split_c);
-  else
-    hipLaunchKernelGGL(split_sum<1>, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, st, ws, O,
-                       n, p.split_c);
-  return hipGetLastError();
+  switch (p.K) {
+    case 1: return launch_valu_k<1>(p, I, F, O, a, st);
+    case 2: return launch_valu_k<2>(p, I, F, O, a, st);
+    case 3: return launch_valu_k<3>(p, I, F, O, a, st);
+    case 4: return launch_valu_k<4>(p, I, F, O, a, st);
+    case 5: return launch_valu_k<5>(p, I, F, O, a, st);
+    case 6: return launch_valu_k<6>(p, I, F, O, a, st);
+    case 7: return launch_valu_k<7>(p, I, F, O, a, st);
+    default: return launch_valu_k<0>(p, I, F, O, a, st);
+  }
 }
 
 }  // namespace dconv

@@ -25,7 +25,6 @@ EINVAL = -2
 ERANGE = -3
 EHIP = -4
 EUNSUPPORTED = -5
-ENOMEM = -6
 
 VARIANT_AUTO = 0
 VARIANT_VALU = 1
@@ -41,8 +40,8 @@ EXPORTED = ("dconv_single", "dconv_single_variant", "dconv_multi", "dconv_multi_
 class Plan(ctypes.Structure):
     """Mirror of ``dconv_plan`` in ``include/dconv.h``."""
     _fields_ = [(n, ctypes.c_int) for n in (
-        "variant", "kernel", "tile_m", "tile_h", "tile_w", "chunk_c", "split_c",
-        "grid_x", "grid_y", "grid_z", "block", "lds_bytes")] + [("workspace_bytes", ctypes.c_longlong)]
+        "variant", "kernel", "tile_m", "tile_h", "tile_w", "chunk_c", "waves_c",
+        "grid_x", "grid_y", "grid_z", "block", "lds_bytes")]
 
     def as_dict(self):
         return {n: getattr(self, n) for n, _ in self._fields_}

@@ -1,0 +1,111 @@
+"""Peak-rate microbenchmarks on the current HIP device (libdconv_peaks.so).
+
+Each function launches one kernel of ``peaks/peaks.hip`` a few times on the
+current torch stream, times the launches with HIP events and returns the
+rate.  These are the measured ceilings the roofline fractions of bench.py
+are reported against beside the datasheet peaks: HBM read, write and copy
+streams, one fp32 FMA per lane per clock (packed fp32 is disabled in this
+build), the two fp32 matrix instructions the convolution kernels use, and
+the global-to-LDS copy path their stages go through.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libdconv_peaks.so")
+_lib = None
+
+
+def load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError("libdconv_peaks.so is not built; run paper_2212_00404_amd/build.py")
+        lib = ctypes.CDLL(LIB_PATH)
+        vp, i, ll = ctypes.c_void_p, ctypes.c_int, ctypes.c_longlong
+        lib.peaks_hbm_read.argtypes = [vp, ll, vp, i, vp]
+        lib.peaks_hbm_write.argtypes = [vp, ll, i, vp]
+        lib.peaks_hbm_copy.argtypes = [vp, vp, ll, i, vp]
+        lib.peaks_fma.argtypes = [vp, i, i, vp]
+        lib.peaks_mfma.argtypes = [vp, i, i, i, vp]
+        lib.peaks_lds_dma.argtypes = [vp, ll, i, i, i, vp, i, vp]
+        for f in ("peaks_hbm_read", "peaks_hbm_write", "peaks_hbm_copy", "peaks_fma",
+                  "peaks_mfma", "peaks_lds_dma"):
+            getattr(lib, f).restype = i
+        _lib = lib
+    return _lib
+
+
+def _time(launch, reps):
+    """Median of `reps` event-timed launches (ms), after one warm-up."""
+    s = torch.cuda.current_stream()
+    launch(s)
+    torch.cuda.synchronize()
+    out = []
+    for _ in range(reps):
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record(s)
+        launch(s)
+        b.record(s)
+        torch.cuda.synchronize()
+        out.append(a.elapsed_time(b))
+    out.sort()
+    return out[len(out) // 2]
+
+
+def _rc(rc):
+    if rc != 0:
+        raise RuntimeError("peaks launch failed (%d)" % rc)
+
+
+def run(reps: int = 10, hbm_mib: int = 2048) -> dict:
+    """Every microbenchmark once; returns a dict of rates."""
+    lib = load()
+    dev = torch.device("cuda", torch.cuda.current_device())
+    cu = torch.cuda.get_device_properties(dev).multi_processor_count
+    sp = lambda s: ctypes.c_void_p(s.cuda_stream)
+    res = {"compute_units": cu}
+    nbytes = hbm_mib << 20
+    a = torch.empty(nbytes // 4, dtype=torch.float32, device=dev).uniform_()
+    b = torch.empty_like(a)
+    grid = cu * 8
+    sink = torch.empty(grid * 256, dtype=torch.float32, device=dev)
+    ms = _time(lambda s: _rc(lib.peaks_hbm_read(a.data_ptr(), nbytes, sink.data_ptr(), grid, sp(s))), reps)
+    res["hbm_read_gbs"] = round(nbytes / ms / 1e6, 1)
+    ms = _time(lambda s: _rc(lib.peaks_hbm_write(b.data_ptr(), nbytes, grid, sp(s))), reps)
+    res["hbm_write_gbs"] = round(nbytes / ms / 1e6, 1)
+    ms = _time(lambda s: _rc(lib.peaks_hbm_copy(a.data_ptr(), b.data_ptr(), nbytes, grid, sp(s))), reps)
+    res["hbm_copy_gbs"] = round(2 * nbytes / ms / 1e6, 1)
+    res["hbm_bytes"] = nbytes
+    del a, b
+    # fp32 FMA: grid x 256 lanes x iters x 8 FMAs x 2 flops
+    iters = 20000
+    grid = cu * 8
+    out = torch.empty(grid * 256, dtype=torch.float32, device=dev)
+    ms = _time(lambda s: _rc(lib.peaks_fma(out.data_ptr(), iters, grid, sp(s))), reps)
+    res["fma_fp32_tflops"] = round(grid * 256 * iters * 8 * 2 / ms / 1e9, 2)
+    # fp32 MFMA: grid x 4 waves x iters x 4 instructions x (4096 or 2048) flops
+    for shape, fl in ((32, 4096), (16, 2048)):
+        it = 4000 if shape == 32 else 8000
+        ms = _time(lambda s: _rc(lib.peaks_mfma(out.data_ptr(), it, grid, shape, sp(s))), reps)
+        res["mfma_f32_%dx%d_tflops" % (shape, shape)] = round(grid * 4 * it * 4 * fl / ms / 1e9, 2)
+    # global -> LDS copies from a 2 MiB region (L2-resident): bytes per
+    # second in total and per compute unit per clock at 2.4 GHz
+    # (16-byte copies also from sources one float off their alignment)
+    region = 1 << 19
+    src = torch.rand(region + 4, dtype=torch.float32, device=dev)
+    g = cu * 2
+    o = torch.empty(g * 256, dtype=torch.float32, device=dev)
+    for width, shift in ((4, 0), (16, 0), (16, 1)):
+        bursts = 400
+        ms = _time(lambda s: _rc(lib.peaks_lds_dma(src.data_ptr(), region, shift, width, bursts,
+                                                   o.data_ptr(), g, sp(s))), reps)
+        total = g * 4 * bursts * 16 * 64 * width
+        key = "lds_dma_b%d%s" % (width * 8, "_unaligned" if shift else "")
+        res[key + "_gbs"] = round(total / ms / 1e6, 1)
+        res[key + "_bytes_per_cu_clk"] = round(total / ms / 1e-3 / cu / 2.4e9, 1)
+    return res

@@ -88,8 +88,20 @@ def test_range_limits():
     assert lib.dconv_single(P, P, P, 40000, 40000, 1, 2, None) == dc.dconv.ERANGE
 
 
+def test_library_allocates_no_device_memory():
+    """The ABI promises no device allocation: the library imports no HIP
+    allocator (hipMalloc*, hipFree*, hipExtMalloc*, memory pools)."""
+    import subprocess
+    out = subprocess.run(["nm", "-D", "--undefined-only", dc.dconv.LIB_PATH],
+                         capture_output=True, text=True, check=True).stdout
+    imported = [l.split()[-1] for l in out.splitlines() if l.strip()]
+    assert imported, "no imported symbols found"
+    bad = [s for s in imported if re.match(r"hip(Ext)?(Malloc|Free|MemPool|HostAlloc|MallocAsync)", s)]
+    assert bad == [], bad
+
+
 def test_strerror():
-    for code in (0, -1, -2, -3, -4, -5, -6):
+    for code in (0, -1, -2, -3, -4, -5):
         assert dc.strerror(code) and dc.strerror(code) != "unknown status"
     assert dc.strerror(12345) == "unknown status"
 
@@ -121,10 +133,11 @@ def _check_multi_plan(C, M, Wx, Wy, K, variant="auto"):
         return p
     tiles = -(-Hout // p["tile_h"]) * -(-Wout // p["tile_w"])
     mtiles = -(-M // p["tile_m"])
-    assert p["grid_x"] == tiles * mtiles * p["split_c"]
-    cps = -(-C // p["split_c"])
-    assert cps <= C or p["split_c"] == 1
-    assert p["workspace_bytes"] == (p["split_c"] * M * Hout * Wout * 4 if p["split_c"] > 1 else 0)
+    # one workgroup per (output tile, filter tile): the channel sum is never
+    # divided among workgroups, only among the waves of one
+    assert p["grid_x"] == tiles * mtiles
+    assert p["waves_c"] >= 1 and p["block"] % (64 * p["waves_c"]) == 0
+    assert p["block"] <= 1024
     if variant == "mfma":
         assert p["variant"] == dc.dconv.VARIANT_MFMA
         assert p["tile_h"] * p["tile_w"] <= 128
@@ -187,20 +200,23 @@ def test_mfma_refuses_large_filters():
         dc.plan_multi(4, 4, 20, 20, 9, "mfma")
 
 
-def test_split_test_shapes_still_split():
-    """The GPU tests of the channel-split machinery need plans that split."""
+def test_wave_split_test_shapes_split_inside_the_workgroup():
+    """The GPU tests of the in-workgroup channel split (several waves summing
+    one output, added through LDS) need plans that take it."""
     import split_shapes
     for s in split_shapes.THREADS + split_shapes.TWO_STREAMS:
-        assert dc.plan_multi(*s)["split_c"] > 1, s
-    assert sum(dc.plan_multi(*s)["split_c"] > 1 for s in split_shapes.REUSE) >= 3
+        assert dc.plan_multi(*s)["waves_c"] > 1, s
+    assert sum(dc.plan_multi(*s)["waves_c"] > 1 for s in split_shapes.REUSE) >= 3
 
 
-def test_small_maps_split_the_channel_sum():
-    """7x7 outputs with 512 channels give far fewer tiles than compute units:
-    the planner must split the channel sum across workgroups."""
+def test_small_maps_take_small_tiles_and_many_waves():
+    """7x7 outputs with 512 channels and filters: without dividing the
+    channel sum among workgroups, filling the chip takes small tiles (at most
+    16 filters x 16 pixels) and many waves per workgroup on the channel sum."""
     p = dc.plan_multi(512, 512, 9, 9, 3)
-    assert p["split_c"] > 1
-    assert p["grid_x"] >= 256
+    assert p["tile_m"] * p["tile_h"] * p["tile_w"] <= 256
+    assert p["waves_c"] >= 8
+    assert p["grid_x"] >= 128
 
 
 @pytest.mark.parametrize("shape", SINGLE_RANDOM, ids=[str(s) for s in SINGLE_RANDOM])

@@ -100,8 +100,9 @@ MULTI_SHAPES = [
     (17, 70, 23, 19, 5), (9, 31, 16, 30, 6), (4, 65, 25, 25, 7), (6, 9, 20, 20, 9),
     (3, 4, 17, 21, 11), (2, 3, 40, 40, 31), (33, 129, 15, 15, 3), (64, 64, 7, 7, 7),
     (3, 64, 70, 70, 7), (130, 7, 9, 9, 3), (1, 96, 100, 3, 3),
-    # one or a few outputs per filter and many channels: the channel sum is
-    # split over up to 64 workgroups (vector and scalar split-sum paths)
+    # one or a few outputs per filter and many channels: long channel sums
+    # inside one workgroup, split over its waves (a channel count that is
+    # not a multiple of any stage leaves a partial last stage)
     (1024, 32, 3, 3, 3), (1536, 32, 4, 5, 3), (1025, 33, 3, 3, 3),
 ]
 
@@ -139,14 +140,41 @@ def test_delta_filter_is_bit_exact_on_random_floats():
     assert np.array_equal(O[1], I[0, 6:40, 0:44])
 
 
-@pytest.mark.parametrize("name", ["multi_c512_9x9_m512_k3", "single_64x64_m1_k3"])
+@pytest.mark.parametrize("name", ["multi_c512_9x9_m512_k3", "multi_c512_16x16_m512_k3",
+                                  "single_64x64_m1_k3", "single_4096x4096_m1_k7"])
 def test_repeated_calls_are_bitwise_identical(name):
-    """Fixed summation order (including the cross-workgroup channel split)."""
+    """Fixed summation order: twenty calls give the same bits (the 7x7 and
+    14x14 layers split every stage's channels over the waves of a workgroup
+    and add them through LDS)."""
+    w = WORKLOADS[name]
+    if w.kind == "multi":
+        assert dc.plan_multi(w.C, w.M, w.Wx, w.Wy, w.K)["waves_c"] > 1
     I, F = make(name)
-    run = gpu_single if WORKLOADS[name].kind == "single" else gpu_multi
-    first = run(I, F)
-    for _ in range(5):
-        assert np.array_equal(run(I, F), first)
+    dev = torch.device("cuda:0")
+    It, Ft = torch.from_numpy(I).to(dev), torch.from_numpy(F).to(dev)
+    run = (lambda: dc.single(It, Ft)) if w.kind == "single" else (lambda: dc.multi(It, Ft))
+    first = run()
+    outs = [run() for _ in range(19)]
+    torch.cuda.synchronize()
+    for o in outs:
+        assert torch.equal(o, first)
+
+
+def test_every_wave_split_plan_is_deterministic():
+    """Every candidate plan with several wave groups on the channel sum,
+    twenty times on the same float data: identical bits each time."""
+    C, M, Wx, Wy, K = 256, 48, 9, 9, 3
+    I, F = random_arrays(C, M, Wx, Wy, K, seed=777)
+    dev = torch.device("cuda:0")
+    It, Ft = torch.from_numpy(I).to(dev), torch.from_numpy(F).to(dev)
+    plans = [p for p in dc.plan_multi_candidates(C, M, Wx, Wy, K) if p["waves_c"] > 1]
+    assert len(plans) >= 4
+    for p in plans:
+        first = dc.multi(It, Ft, plan=p)
+        outs = [dc.multi(It, Ft, plan=p) for _ in range(19)]
+        torch.cuda.synchronize()
+        for o in outs:
+            assert torch.equal(o, first), p
 
 
 def test_every_output_written_on_a_side_stream():
@@ -171,13 +199,12 @@ def test_every_output_written_on_a_side_stream():
     assert_within(outs.cpu().numpy(), O64, A64, "side stream single")
 
 
-def test_split_workspace_reused_across_plans():
-    """Channel-split calls with different tile counts and split factors queued
-    back to back on one stream share its workspace: the arrival counters must
-    be back at zero after every call, and growth between calls must not
-    disturb queued work."""
+def test_wave_split_plans_back_to_back():
+    """Calls with different plans (with and without the in-workgroup split of
+    the channel sum) queued back to back on one stream: each leaves nothing
+    behind that the next one reads."""
     shapes = split_shapes.REUSE
-    splits = [dc.plan_multi(*s)["split_c"] for s in shapes]
+    splits = [dc.plan_multi(*s)["waves_c"] for s in shapes]
     assert sum(sp > 1 for sp in splits) >= 3, splits
     cases = []
     for i, (C, M, Wx, Wy, K) in enumerate(shapes):
@@ -191,10 +218,10 @@ def test_split_workspace_reused_across_plans():
         assert_exact(out.cpu().numpy(), O64, "reuse %r" % (s,))
 
 
-def test_split_calls_on_two_streams():
-    """Concurrent channel-split calls on two streams use separate workspaces."""
+def test_wave_split_calls_on_two_streams():
+    """Wave-split calls on two streams at once share nothing but the device."""
     shapes = split_shapes.TWO_STREAMS
-    assert all(dc.plan_multi(*s)["split_c"] > 1 for s in shapes)
+    assert all(dc.plan_multi(*s)["waves_c"] > 1 for s in shapes)
     data = [random_arrays(*s, seed=9100 + i, variant="int") for i, s in enumerate(shapes)]
     dev = [(torch.from_numpy(I).cuda(), torch.from_numpy(F).cuda()) for I, F in data]
     streams = [torch.cuda.Stream(), torch.cuda.Stream()]
@@ -212,14 +239,14 @@ def test_split_calls_on_two_streams():
 
 
 def test_calls_from_several_host_threads():
-    """Four host threads, each with its own stream, issue channel-split and
-    single-map calls at once (the C calls run without the Python lock): the
-    per-(device, stream) workspaces and the planner are shared state, and
-    every result must still be exact."""
+    """Four host threads, each with its own stream, issue wave-split
+    multi-channel and single-map calls at once (the C calls run without the
+    Python lock): the property cache and the planners are shared, and every
+    result must still be exact."""
     import threading
 
     shapes = split_shapes.THREADS
-    assert all(dc.plan_multi(*s)["split_c"] > 1 for s in shapes)
+    assert all(dc.plan_multi(*s)["waves_c"] > 1 for s in shapes)
     data = [random_arrays(*s, seed=9200 + i, variant="int") for i, s in enumerate(shapes)]
     Is, Fs = random_arrays(1, 3, 300, 200, 5, seed=9300, variant="int")
     dev = torch.device("cuda:0")
@@ -254,3 +281,64 @@ def test_calls_from_several_host_threads():
         for om, osg in outs[k]:
             assert_exact(om.cpu().numpy(), O64, "thread %d multi" % k)
             assert_exact(osg.cpu().numpy(), O64s, "thread %d single" % k)
+
+
+def _offset_view(host, offset, dev, guard=4):
+    """A contiguous device view of `host` whose first element sits `offset`
+    floats past a fresh allocation (so 4 * offset bytes off its alignment),
+    with NaN in the `offset` floats before it and `guard` floats after it."""
+    flat = torch.full((offset + host.size + guard,), float("nan"), dtype=torch.float32, device=dev)
+    view = flat[offset:offset + host.size].view(host.shape)
+    view.copy_(torch.from_numpy(np.ascontiguousarray(host)))
+    return flat, view
+
+
+def _guards_intact(flat, offset, n):
+    f = flat.cpu().numpy()
+    return np.isnan(f[:offset]).all() and np.isnan(f[offset + n:]).all()
+
+
+# (offset of I, of F, of O) in floats: every base address off 16-byte
+# alignment in turn, and all three at once
+OFFSETS = [(1, 2, 3), (0, 0, 1), (0, 0, 2), (2, 0, 0), (3, 1, 0), (1, 1, 1)]
+
+
+@pytest.mark.parametrize("offsets", OFFSETS, ids=[str(o) for o in OFFSETS])
+def test_misaligned_base_pointers(offsets):
+    """I, F and O passed as views whose base pointers are 4, 8 or 12 bytes
+    off a 16-byte boundary (the planners choose float4 staging, the
+    matrix-core single-map kernel and the store kind from the pointers'
+    alignment): results match the oracle and nothing outside O is written."""
+    oi, of, oo = offsets
+    dev = torch.device("cuda:0")
+    # single map: float4 and single-float staging, non-temporal and ordinary
+    # stores (four filters per workgroup and 64 MB of output), matrix cores
+    for (Wx, Wy, K, M) in [(300, 70, 5, 3), (1024, 1024, 3, 16), (260, 40, 7, 2)]:
+        I, F = random_arrays(1, M, Wx, Wy, K, seed=Wx * 31 + K + 17 * oi + of, variant="int")
+        I, F = I[0], F[:, 0]
+        O64, _ = oracle_single(I, F)
+        _, It = _offset_view(I, oi, dev)
+        _, Ft = _offset_view(F, of, dev)
+        for fam in single_families(Wx, K):
+            flat, Ot = _offset_view(np.zeros(O64.shape, np.float32), oo, dev)
+            if fam == "mfma" and oi % 4:
+                # the matrix-core kernel stages whole 16-byte rows
+                with pytest.raises(RuntimeError, match="cannot run"):
+                    dc.single(It, Ft, out=Ot, variant=fam)
+                continue
+            dc.single(It, Ft, out=Ot, variant=fam)
+            torch.cuda.synchronize()
+            assert_exact(Ot.cpu().numpy(), O64, "single %r %s %r" % ((Wx, Wy, K, M), fam, offsets))
+            assert _guards_intact(flat, oo, O64.size), "single wrote outside O"
+    for (C, M, Wx, Wy, K) in [(33, 70, 23, 19, 3), (256, 40, 9, 9, 3), (20, 24, 14, 13, 1),
+                              (6, 9, 20, 20, 9)]:
+        I, F = random_arrays(C, M, Wx, Wy, K, seed=C * 131 + K + 7 * oo, variant="int")
+        O64, _ = oracle_multi(I, F)
+        _, It = _offset_view(I, oi, dev)
+        _, Ft = _offset_view(F, of, dev)
+        for fam in ["auto", "valu"] + (["mfma"] if K <= 7 else []):
+            flat, Ot = _offset_view(np.zeros(O64.shape, np.float32), oo, dev)
+            dc.multi(It, Ft, out=Ot, variant=fam)
+            torch.cuda.synchronize()
+            assert_exact(Ot.cpu().numpy(), O64, "multi %r %s %r" % ((C, M, Wx, Wy, K), fam, offsets))
+            assert _guards_intact(flat, oo, O64.size), "multi wrote outside O"

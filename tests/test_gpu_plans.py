@@ -1,5 +1,5 @@
 """GPU: every multi-channel plan the library can run (each workgroup shape
-crossed with each channel split, both kernel families) against the oracle,
+of both kernel families) against the oracle,
 plans chosen by the caller, and the latency probe behind the paper's model.
 Integer data, so every plan must be bit-exact (every
 summation order of small integers is exact in fp32)."""
@@ -46,7 +46,7 @@ def test_foreign_plan_is_rejected():
     I, F = random_arrays(C, M, Wx, Wy, K, seed=1)
     It, Ft = torch.from_numpy(I).cuda(), torch.from_numpy(F).cuda()
     p = dict(dc.plan_multi(C, M, Wx, Wy, K))
-    for field, delta in (("grid_x", 1), ("split_c", 1), ("tile_m", 32), ("kernel", 7)):
+    for field, delta in (("grid_x", 1), ("waves_c", 1), ("tile_m", 32), ("kernel", 7)):
         bad = dict(p, **{field: p[field] + delta})
         with pytest.raises(RuntimeError, match="invalid"):
             dc.multi(It, Ft, plan=bad)

@@ -150,7 +150,7 @@ def test_candidates_cover_the_planner_and_fit(layer):
     Hout, Wout = Wy - K + 1, Wx - K + 1
     seen = set()
     for p in cands:
-        key = (p["variant"], p["kernel"], p["split_c"])
+        key = (p["variant"], p["kernel"])
         assert key not in seen
         seen.add(key)
         assert p["lds_bytes"] <= 160 * 1024
@@ -158,9 +158,7 @@ def test_candidates_cover_the_planner_and_fit(layer):
             assert p["grid_x"] * p["block"] >= M * Hout * Wout
             continue
         tiles = -(-Hout // p["tile_h"]) * -(-Wout // p["tile_w"])
-        assert p["grid_x"] == tiles * -(-M // p["tile_m"]) * p["split_c"]
-        assert p["workspace_bytes"] == (p["split_c"] * M * Hout * Wout * 4
-                                        if p["split_c"] > 1 else 0)
+        assert p["grid_x"] == tiles * -(-M // p["tile_m"])
 
 
 @pytest.mark.parametrize("layer", MULTI_LAYERS)
@@ -170,15 +168,15 @@ def test_paper_rule_plan(layer):
     p = dc.plan_multi_paper(C, M, Wx, Wy, K, dev)
     cands = dc.plan_multi_candidates(C, M, Wx, Wy, K)
     assert p in cands
-    assert p["split_c"] == 1          # the paper keeps the channel sum on one processor
     n_fma = dc.model_latency(dev)["n_fma"]
-    unsplit = [c for c in cands if c["split_c"] == 1]
+    unsplit = cands   # no plan divides the channel sum among workgroups
 
     def work(c):
         if c["kernel"] == 99:
             return 0
         per_wg = c["tile_m"] * c["chunk_c"] * K * K * c["tile_h"] * c["tile_w"]
-        occ = min(8, dev["onchip_bytes"] // c["lds_bytes"] if c["lds_bytes"] else 8,
+        max_wg = 2048 // c["block"]
+        occ = min(max_wg, dev["onchip_bytes"] // c["lds_bytes"] if c["lds_bytes"] else max_wg,
                   -(-c["grid_x"] // dev["num_cu"]))
         return per_wg * max(occ, 1)
 
