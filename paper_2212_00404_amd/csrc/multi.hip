@@ -119,6 +119,13 @@ __device__ __forceinline__ void lds_barrier() {
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
 
+// Direct global->LDS copy of 16 bytes per lane: lane l's four floats from
+// src land at lds_row[4l .. 4l+3]; lds_row must be wave-uniform and 4-byte
+// aligned (a 16-byte boundary is not needed), src 4-byte aligned.
+__device__ __forceinline__ void dma_f128(const float *src, float *lds_row) {
+  __builtin_amdgcn_global_load_lds(src, (lds_void_ptr)lds_row, 16, 0, 0);
+}
+
 // Wait until this wave's direct global->LDS loads have landed in LDS.
 __device__ __forceinline__ void wait_lds_dma() { asm volatile("s_waitcnt vmcnt(0)" ::: "memory"); }
 
@@ -311,24 +318,37 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     const int gx = min(px0 + (e - iy * a.IW), a.Wx - 1);
     ioff[j] = gy * a.Wx + gx;
   }
-  // Filter rows are copied in 64-lane chunks; chunk q of a row covers row
-  // elements [64q, 64q+64).  When the last chunk's overhang stays within the
-  // next row's slot (FSPILL), its lanes past FROW land on the row's padding
-  // float or at position e of the next row's slot and copy that row's element
-  // e (element 0 for a padding float): they write what the next row's own
-  // copy writes, so the order of the two copies does not matter.  For the
-  // last row of a wave's block they land in the gap after the block and
-  // re-read the row's first element.  Otherwise the last chunk is masked.
-  constexpr bool FSPILL = 64 * NCF <= 2 * FP;
+  // Filter rows.  Rows of at least 256 floats whose length is a multiple of
+  // 4 (F128) start with NF4 16-byte-per-lane copies (1 KB per instruction,
+  // about 1.6x the bytes per clock of 4-byte copies), chunk q covering row
+  // elements [256q, 256q+256); the rest of a row, from T = 256 * NF4, goes in
+  // NT 64-lane chunks of 4-byte copies.  The last chunk's lanes past FROW
+  // land on the row's padding float or at position e of the next row's slot
+  // and copy that row's element e (element 0 for a padding float): they
+  // write what the next row's own copy writes, so the order of the two
+  // copies does not matter.  For the last row of a wave's block they land
+  // in the 64-float gap after the block and re-read the row's first
+  // element.  Every copy runs on all 64 lanes (each lane picks its source),
+  // with no branch around it.
+  constexpr bool F128 = FROW % 4 == 0 && FROW >= 256;
+  constexpr int NF4 = F128 ? FROW / 256 : 0;
+  constexpr int T = 256 * NF4;
+  constexpr int NT = ceil_div(FROW - T, 64);
+  // The overhang stays within the next row's elements (short rows: the last
+  // chunk is masked instead) and, for a block's last row, within the gap.
+  constexpr bool FSPILL = T + 64 * NT <= FROW + FP;
+  static_assert(T + 64 * NT <= FP + 64, "overhang of a block's last row fits the gap");
   const size_t plane_elems = (size_t)a.Wy * a.Wx;
   // PAIR: lanes 32-63 copy the next channel's plane
   const size_t pair_off = PAIR ? (size_t)(lane >> 5) * plane_elems : 0;
   const size_t frow_stride = (size_t)a.C * KK;
-  const int e_last = 64 * (NCF - 1) + lane;
+  const int e_last = T + 64 * (NT - 1) + lane;
   const bool f_spill = e_last >= FROW;
   int e_next = e_last - FP;
   if (e_next < 0 || e_next >= FROW) e_next = 0;
-  const int ofs_last = f_spill ? (int)frow_stride + e_next : e_last;
+  // source of the last chunk relative to the row start: within a block
+  // (times the row distance for the spilling lanes), and for its last row
+  const int ofs_last = f_spill ? e_next : e_last;
   const int ofs_last_end = f_spill ? 0 : e_last;
 
   acc_t acc[MB][NB];
@@ -345,43 +365,30 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   auto issue = [&](int c0, float *buf) {
     const int nc = min(CC, c_end - c0);
     if (nc == CC) {
-      // This wave's RPW consecutive filter rows, in ascending order.  The
-      // last chunk of a row may spill past FROW into the next row's first
-      // elements; copies from one wave land in issue order, so the next
-      // row's own copy (issued later) overwrites the spill, and the last
-      // row of the block spills into the 64-float gap after it.  Rows past M
-      // (last filter tile only) are clamped to filter M-1: they only feed
-      // outputs that are never stored.
+      // This wave's RPW consecutive filter rows, in ascending order.  Rows
+      // past M (last filter tile only) are clamped to filter M-1: they only
+      // feed outputs that are never stored; a clamped row's spilling lanes
+      // re-read that same row, which is also what the next slot holds.
       float *dst = buf + wave * FBLK;
       const int r0 = m0 + wave * RPW;
-      if (r0 + RPW <= a.M) {
-        const float *src = F + ((size_t)r0 * a.C + c0) * KK;
 #pragma unroll
-        for (int i = 0; i < RPW; ++i) {
+      for (int i = 0; i < RPW; ++i) {
+        const int rr = min(r0 + i, a.M - 1);
+        const int rn = min(r0 + i + 1, a.M - 1);
+        const float *src = F + ((size_t)rr * a.C + c0) * KK;
 #pragma unroll
-          for (int q = 0; q < NCF - 1; ++q) dma_f32(src + 64 * q + lane, dst + 64 * q);
-          if constexpr (FSPILL)
-            dma_f32(src + (i + 1 < RPW ? ofs_last : ofs_last_end), dst + 64 * (NCF - 1));
-          else if (!f_spill)
-            dma_f32(src + e_last, dst + 64 * (NCF - 1));
-          src += frow_stride;
-          dst += FP;
+        for (int q = 0; q < NF4; ++q) dma_f128(src + 256 * q + 4 * lane, dst + 256 * q);
+#pragma unroll
+        for (int q = 0; q < NT - 1; ++q) dma_f32(src + T + 64 * q + lane, dst + T + 64 * q);
+        if constexpr (FSPILL) {
+          const size_t ofs = i + 1 < RPW
+                                 ? (f_spill ? (size_t)(rn - rr) * frow_stride : 0) + (size_t)ofs_last
+                                 : (size_t)ofs_last_end;
+          dma_f32(src + ofs, dst + T + 64 * (NT - 1));
+        } else if (!f_spill) {
+          dma_f32(src + e_last, dst + T + 64 * (NT - 1));
         }
-      } else {
-#pragma unroll
-        for (int i = 0; i < RPW; ++i) {
-          const int rr = min(r0 + i, a.M - 1);
-          const int rn = min(r0 + i + 1, a.M - 1);
-          const float *src = F + ((size_t)rr * a.C + c0) * KK;
-#pragma unroll
-          for (int q = 0; q < NCF - 1; ++q) dma_f32(src + 64 * q + lane, dst + 64 * q);
-          const size_t spill = (i + 1 < RPW) ? (size_t)(rn - rr) * frow_stride + e_next : 0;
-          if constexpr (FSPILL)
-            dma_f32(src + (f_spill ? spill : (size_t)e_last), dst + 64 * (NCF - 1));
-          else if (!f_spill)
-            dma_f32(src + e_last, dst + 64 * (NCF - 1));
-          dst += FP;
-        }
+        dst += FP;
       }
       if constexpr (PAIR) {
         // channel pairs (cl, cl + 1), cl even; CC is even

@@ -33,8 +33,9 @@ def load():
         lib.peaks_fma.argtypes = [vp, i, i, vp]
         lib.peaks_mfma.argtypes = [vp, i, i, i, vp]
         lib.peaks_lds_dma.argtypes = [vp, ll, i, i, i, vp, i, vp]
+        lib.peaks_lds_dma_layout.argtypes = [vp, i, i, vp, vp]
         for f in ("peaks_hbm_read", "peaks_hbm_write", "peaks_hbm_copy", "peaks_fma",
-                  "peaks_mfma", "peaks_lds_dma"):
+                  "peaks_mfma", "peaks_lds_dma", "peaks_lds_dma_layout"):
             getattr(lib, f).restype = i
         _lib = lib
     return _lib
@@ -109,3 +110,17 @@ def run(reps: int = 10, hbm_mib: int = 2048) -> dict:
         res[key + "_gbs"] = round(total / ms / 1e6, 1)
         res[key + "_bytes_per_cu_clk"] = round(total / ms / 1e-3 / cu / 2.4e9, 1)
     return res
+
+
+def lds_dma_layout(shift: int, active: int = 64):
+    """The 264-float LDS array after one wave's 16-byte-per-lane direct copy
+    of 256 floats (1, 2, ..., 256) to float offset `shift`, issued by lanes
+    0 .. active-1 only (see peaks.hip)."""
+    lib = load()
+    dev = torch.device("cuda", torch.cuda.current_device())
+    src = torch.arange(256, dtype=torch.float32, device=dev) + 1.0
+    out = torch.full((264,), -1.0, dtype=torch.float32, device=dev)
+    _rc(lib.peaks_lds_dma_layout(src.data_ptr(), shift, active, out.data_ptr(),
+                                 ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)))
+    torch.cuda.synchronize()
+    return out.cpu()

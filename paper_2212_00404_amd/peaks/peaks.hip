@@ -145,7 +145,36 @@ __global__ __launch_bounds__(256) void lds_dma_stream(const float *__restrict__ 
   out[(int64_t)blockIdx.x * 256 + threadIdx.x] = buf[threadIdx.x];
 }
 
+// Where a 16-byte-per-lane direct copy lands when its LDS destination is
+// `shift` floats (0 to 3) past a 16-byte boundary: one wave copies 256
+// floats of src into a zeroed LDS array at float offset shift, then writes
+// the whole array (264 floats) to out.  Lane l's four floats are expected at
+// shift + 4l .. shift + 4l + 3.
+// With active < 64 only lanes 0 .. active-1 issue the copy (the others are
+// masked off by a branch), which shows what masked-off lanes write.
+__global__ __launch_bounds__(64) void lds_dma_layout(const float *__restrict__ src, int shift,
+                                                     int active, float *__restrict__ out) {
+  __shared__ __attribute__((aligned(16))) float buf[264];
+  const int lane = threadIdx.x;
+  for (int i = lane; i < 264; i += 64) buf[i] = 0.f;
+  __syncthreads();
+  if (lane < active)
+    __builtin_amdgcn_global_load_lds(src + 4 * lane, (lds_void_ptr)(buf + shift), 16, 0, 0);
+  asm volatile("s_waitcnt vmcnt(0)" ::: "memory");
+  __syncthreads();
+  for (int i = lane; i < 264; i += 64) out[i] = buf[i];
+}
+
 }  // namespace
+
+PEAKS_EXPORT int peaks_lds_dma_layout(const float *src, int shift, int active, float *out,
+                                      void *stream) {
+  if (!src || !out || shift < 0 || shift > 3 || active < 1 || active > 64) return -1;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(lds_dma_layout, dim3(1), dim3(64), 0, (hipStream_t)stream, src, shift, active,
+                     out);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
 
 // All calls: enqueue on `stream` and return 0, or -1 for a bad argument, or
 // -4 if the launch failed.  `sink` / `out` hold grid x 256 floats.
