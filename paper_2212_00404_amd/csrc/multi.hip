@@ -30,6 +30,7 @@
 //   * VALU: one output pixel per lane and MR filters per wave, with the
 //     filter values wave-uniform in scalar registers and one fp32 FMA per
 //     term (packed fp32 FMAs are not used).
+#include <type_traits>
 #include <utility>
 #include <vector>
 
@@ -235,6 +236,17 @@ struct MfmaCfg {
   static_assert(MT % NW == 0, "filter rows are shared out over the waves");
 };
 
+// fn(integral_constant<int, B>), fn(... B + 1), ..., fn(... E - 1).
+template <int B, int E, class Fn>
+__device__ __forceinline__ void static_for(Fn &&fn) {
+  if constexpr (B < E) {
+    fn(std::integral_constant<int, B>{});
+    static_for<B + 1, E>(fn);
+  }
+}
+
+
+
 // Stage pipeline: while the MFMAs consume stage s from one LDS buffer, the
 // filter slice and input tile of stage s+1 stream into the other buffer with
 // direct global->LDS loads (no registers, no LDS write instructions).  The
@@ -359,95 +371,108 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 #pragma unroll
       for (int v = 0; v < NV; ++v) acc[mb][nb][v] = 0.f;
 
-  // Start the loads of the stage at channel c0 into `buf`: filter row r to
-  // buf[(r / RPW)*FBLK + (r % RPW)*FP + e], input planes to
-  // buf[F_FLOATS + cl*ICS + e].
-  auto issue = [&](int c0, float *buf) {
-    const int nc = min(CC, c_end - c0);
-    if (nc == CC) {
-      // This wave's RPW consecutive filter rows, in ascending order.  Rows
-      // past M (last filter tile only) are clamped to filter M-1: they only
-      // feed outputs that are never stored; a clamped row's spilling lanes
-      // re-read that same row, which is also what the next slot holds.
-      float *dst = buf + wave * FBLK;
-      const int r0 = m0 + wave * RPW;
-#pragma unroll
-      for (int i = 0; i < RPW; ++i) {
-        const int rr = min(r0 + i, a.M - 1);
-        const int rn = min(r0 + i + 1, a.M - 1);
-        const float *src = F + ((size_t)rr * a.C + c0) * KK;
-#pragma unroll
-        for (int q = 0; q < NF4; ++q) dma_f128(src + 256 * q + 4 * lane, dst + 256 * q);
-#pragma unroll
-        for (int q = 0; q < NT - 1; ++q) dma_f32(src + T + 64 * q + lane, dst + T + 64 * q);
-        if constexpr (FSPILL) {
-          const size_t ofs = i + 1 < RPW
-                                 ? (f_spill ? (size_t)(rn - rr) * frow_stride : 0) + (size_t)ofs_last
-                                 : (size_t)ofs_last_end;
-          dma_f32(src + ofs, dst + T + 64 * (NT - 1));
-        } else if (!f_spill) {
-          dma_f32(src + e_last, dst + T + 64 * (NT - 1));
-        }
-        dst += FP;
-      }
-      if constexpr (PAIR) {
-        // channel pairs (cl, cl + 1), cl even; CC is even
-        const float *src = I + (size_t)(c0 + 2 * wave) * plane_elems;
-        for (int cl = 2 * wave; cl < CC; cl += 2 * NW) {
-          dma_f32(src + pair_off + ioff[0], buf + F_FLOATS + cl * ICS);
-          src += 2 * NW * plane_elems;
-        }
+  // The copies of one full stage, as ND slots in a fixed order: the RPW
+  // filter rows of this wave (SF copies each: NF4 16-byte chunks, NT - 1
+  // plain 4-byte chunks, then the last chunk with its overhang), then the
+  // input planes cl = wave, wave + NW, ... (PAIR: pairs from 2 * wave) in
+  // NCI chunks each.
+  //   Filter row r goes to buf[(r / RPW)*FBLK + (r % RPW)*FP + e], input
+  // planes to buf[F_FLOATS + cl*ICS + e].  Rows past M (last filter tile
+  // only) are clamped to filter M-1: they only feed outputs that are never
+  // stored; a clamped row's spilling lanes re-read that same row, which is
+  // also what the next slot holds.
+  constexpr int SF = NF4 + NT;
+  constexpr int ND_F = RPW * SF;
+  constexpr int PL = PAIR ? ceil_div(CC, 2 * NW) : ceil_div(CC, NW);
+  constexpr int ND = ND_F + PL * NCI;
+  auto issue_slot = [&](int c0, float *buf, auto S) __attribute__((always_inline)) {
+    constexpr int s = decltype(S)::value;
+    if constexpr (s < ND_F) {
+      constexpr int i = s / SF, q = s % SF;
+      const int rr = min(m0 + wave * RPW + i, a.M - 1);
+      const float *src = F + ((size_t)rr * a.C + c0) * KK;
+      float *dst = buf + wave * FBLK + i * FP;
+      if constexpr (q < NF4) {
+        dma_f128(src + 256 * q + 4 * lane, dst + 256 * q);
+      } else if constexpr (q < SF - 1) {
+        dma_f32(src + T + 64 * (q - NF4) + lane, dst + T + 64 * (q - NF4));
+      } else if constexpr (FSPILL) {
+        const int rn = min(m0 + wave * RPW + i + 1, a.M - 1);
+        const size_t ofs = i + 1 < RPW
+                               ? (f_spill ? (size_t)(rn - rr) * frow_stride : 0) + (size_t)ofs_last
+                               : (size_t)ofs_last_end;
+        dma_f32(src + ofs, dst + T + 64 * (NT - 1));
       } else {
-        const float *src = I + (size_t)(c0 + wave) * plane_elems;
-        for (int cl = wave; cl < CC; cl += NW) {
-          float *dsti = buf + F_FLOATS + cl * ICS;
-#pragma unroll
-          for (int j = 0; j < NCI; ++j)
-            if (j < nci) dma_f32(src + ioff[j], dsti + 64 * j);
-          src += NW * plane_elems;
-        }
+        if (!f_spill) dma_f32(src + e_last, dst + T + 64 * (NT - 1));
       }
     } else {
-      // Partial stage (the channel range ends inside it): copy the nc
-      // channels present and zero the rest, which meet valid outputs.
-      const int flen = nc * KK;
-      for (int i = 0; i < RPW; ++i) {
-        const int r = wave * RPW + i;
-        const float *src = F + ((size_t)min(m0 + r, a.M - 1) * a.C + c0) * KK + lane;
-        float *dst = buf + wave * FBLK + i * FP;
-        for (int q = 0; q < NCF; ++q)
-          if (64 * q + lane < flen) dma_f32(src + 64 * q, dst + 64 * q);
-      }
+      constexpr int u = s - ND_F, t = u / NCI, jj = u % NCI;
       if constexpr (PAIR) {
-        // the second plane of the last pair only where that channel exists
-        for (int cl = 2 * wave; cl < nc; cl += 2 * NW)
-          if (cl + (lane >> 5) < nc)
-            dma_f32(I + (size_t)(c0 + cl) * plane_elems + pair_off + ioff[0],
-                    buf + F_FLOATS + cl * ICS);
+        // channel pairs (cl, cl + 1), cl even; CC is even
+        const int cl = 2 * wave + t * 2 * NW;
+        if (cl < CC)
+          dma_f32(I + (size_t)(c0 + cl) * plane_elems + pair_off + ioff[0], buf + F_FLOATS + cl * ICS);
       } else {
-        for (int cl = wave; cl < nc; cl += NW) {
-          const float *src = I + (size_t)(c0 + cl) * plane_elems;
-          float *dst = buf + F_FLOATS + cl * ICS;
-#pragma unroll
-          for (int j = 0; j < NCI; ++j)
-            if (j < nci) dma_f32(src + ioff[j], dst + 64 * j);
-        }
+        const int cl = wave + t * NW;
+        if (cl < CC && jj < nci)
+          dma_f32(I + (size_t)(c0 + cl) * plane_elems + ioff[jj], buf + F_FLOATS + cl * ICS + 64 * jj);
       }
-      const int fz = FROW - flen;
-      for (int idx = threadIdx.x; idx < MT * fz; idx += NTHR) {
-        const int r = idx / fz;
-        buf[(r / RPW) * FBLK + (r % RPW) * FP + flen + (idx - r * fz)] = 0.f;
-      }
-      for (int idx = threadIdx.x; idx < (CC - nc) * ICS; idx += NTHR)
-        buf[F_FLOATS + nc * ICS + idx] = 0.f;
     }
+  };
+  auto issue_slots = [&](int c0, float *buf, auto B, auto E) __attribute__((always_inline)) {
+    static_for<decltype(B)::value, decltype(E)::value>([&](auto S) { issue_slot(c0, buf, S); });
+  };
+
+  // Partial stage (the channel range ends inside it): copy the nc channels
+  // present and zero the rest, which meet valid outputs.
+  auto issue_partial = [&](int c0, float *buf) __attribute__((always_inline)) {
+    const int nc = c_end - c0;
+    const int flen = nc * KK;
+    for (int i = 0; i < RPW; ++i) {
+      const int r = wave * RPW + i;
+      const float *src = F + ((size_t)min(m0 + r, a.M - 1) * a.C + c0) * KK + lane;
+      float *dst = buf + wave * FBLK + i * FP;
+      for (int q = 0; q < NCF; ++q)
+        if (64 * q + lane < flen) dma_f32(src + 64 * q, dst + 64 * q);
+    }
+    if constexpr (PAIR) {
+      // the second plane of the last pair only where that channel exists
+      for (int cl = 2 * wave; cl < nc; cl += 2 * NW)
+        if (cl + (lane >> 5) < nc)
+          dma_f32(I + (size_t)(c0 + cl) * plane_elems + pair_off + ioff[0],
+                  buf + F_FLOATS + cl * ICS);
+    } else {
+      for (int cl = wave; cl < nc; cl += NW) {
+        const float *src = I + (size_t)(c0 + cl) * plane_elems;
+        float *dst = buf + F_FLOATS + cl * ICS;
+#pragma unroll
+        for (int j = 0; j < NCI; ++j)
+          if (j < nci) dma_f32(src + ioff[j], dst + 64 * j);
+      }
+    }
+    const int fz = FROW - flen;
+    for (int idx = threadIdx.x; idx < MT * fz; idx += NTHR) {
+      const int r = idx / fz;
+      buf[(r / RPW) * FBLK + (r % RPW) * FP + flen + (idx - r * fz)] = 0.f;
+    }
+    for (int idx = threadIdx.x; idx < (CC - nc) * ICS; idx += NTHR)
+      buf[F_FLOATS + nc * ICS + idx] = 0.f;
+  };
+  // A whole stage at once (the first stages, and partial stages).
+  auto issue = [&](int c0, float *buf) __attribute__((always_inline)) {
+    if (c_end - c0 >= CC)
+      issue_slots(c0, buf, std::integral_constant<int, 0>{}, std::integral_constant<int, ND>{});
+    else
+      issue_partial(c0, buf);
   };
 
   // The stage's k-steps (channel group cg, filter row r, filter column s) run
-  // in chunks of L with one chunk of operand look-ahead from LDS.  The empty
-  // asm statements on the accumulators and the scheduling barriers keep the
-  // compiler from hoisting every LDS read of the stage into registers.
-  auto compute = [&](const float *buf) {
+  // in NCH chunks of L with one chunk of operand look-ahead from LDS.  The
+  // empty asm statements on the accumulators and the scheduling barriers
+  // keep the compiler from hoisting every LDS read of the stage into
+  // registers.  (Issuing the next stage's copies a few at a time between
+  // these chunks instead of all before them measured 3-13% slower.)
+  auto compute = [&](const float *buf) __attribute__((always_inline)) {
     constexpr int NQ = (CCW / KG) * KK;
     constexpr int L = 4;
     constexpr int NCH = (NQ + L - 1) / L;
@@ -466,8 +491,8 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
       }
     };
     load_chunk(0, ca, cb);
-#pragma unroll
-    for (int ch = 0; ch < NCH; ++ch) {
+    static_for<0, NCH>([&](auto CH) {
+      constexpr int ch = decltype(CH)::value;
       // The look-ahead reads are issued between the two halves of this
       // chunk's MFMAs: late enough that waiting for them at the start of the
       // next chunk costs nothing, early enough to be in flight for half a
@@ -498,20 +523,32 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 #pragma unroll
         for (int nb = 0; nb < NB; ++nb) cb[l][nb] = nbv[l][nb];
       }
-    }
+    });
   };
 
+  // Two stage buffers: while stage s is computed from one, the copies of
+  // stage s+1 land in the other.  Before computing a stage, wait for this
+  // wave's copies of it, then the barrier: every wave's copies have landed,
+  // and every wave is done with the other buffer, which the next stage's
+  // copies refill.  Each buffer is named as the LDS object itself where it
+  // is used (not a pointer chosen at run time), which is what lets the
+  // compiler leave the copies to one buffer in flight while the other is
+  // read.  (A third and a fourth buffer, for more loads in flight, measured
+  // no faster on any layer.)
+  auto stage = [&](auto J, int cs) __attribute__((always_inline)) {
+    constexpr int j = decltype(J)::value;
+    float *cur = j == 0 ? buf0 : buf1;
+    float *nxt = j == 0 ? buf1 : buf0;
+    wait_lds_dma();
+    lds_barrier();
+    if (cs + CC < c_end) issue(cs + CC, nxt);
+    compute(cur);
+  };
   issue(0, buf0);
   for (int c0 = 0; c0 < c_end; c0 += 2 * CC) {
-    wait_lds_dma();
-    lds_barrier();  // stage c0 is in buf0; buf1 is free
-    if (c0 + CC < c_end) issue(c0 + CC, buf1);
-    compute(buf0);
+    stage(std::integral_constant<int, 0>{}, c0);
     if (c0 + CC >= c_end) break;
-    wait_lds_dma();
-    lds_barrier();  // stage c0+CC is in buf1; buf0 is free
-    if (c0 + 2 * CC < c_end) issue(c0 + 2 * CC, buf0);
-    compute(buf1);
+    stage(std::integral_constant<int, 1>{}, c0 + CC);
   }
 
   // Fixed-order sum of the WC channel groups through LDS: group 0 adds the
@@ -890,8 +927,10 @@ Candidate valu_candidate(int i) {
 //          co-resident workgroups overlap each other's chains
 //   copy:  the bytes a CU stages into LDS, at the rate one CU's vector
 //          memory path delivers them
-// The constants were fitted to exhaustive timings of every candidate plan of
-// the layer shapes in the benchmark set on an MI355X.
+// The constants were fitted to exhaustive timings of every matrix-core
+// candidate plan of the nineteen benchmark layers on an MI355X (the fitted
+// model picks a plan within 0.3% of the fastest on average, 5% at worst);
+// the MFMA terms are empirical weights, not instruction latencies.
 double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
                 const TileChoice &t, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
@@ -901,14 +940,15 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
   const int kk = K * K;
   // Fitted per family: the matrix-core kernels on every layer with their
   // eight-wave and deep shapes, the vector kernels on the same layers.
-  constexpr double kMfma32Cycles = 80.0;  // one 32x32x2 MFMA per wave (issue: 64)
-  constexpr double kMfma16Cycles = 40.0;  // one 16x16x4 MFMA per wave (issue: 32)
-  constexpr double kOneWavePerSimd = 1.3; // MFMA cycles factor with one wave per SIMD
-  constexpr double kWcReduction = 300.0;  // per extra wave group
+  constexpr double kMfma32Cycles = 64.3;  // one 32x32x2 MFMA per wave (issue: 64)
+  constexpr double kMfma16Cycles = 18.0;  // one 16x16x4 MFMA per wave (issue: 32)
+  constexpr double kOneWavePerSimd = 1.25; // MFMA cycles factor with one wave per SIMD
+  constexpr double kSeveralAcc = 1.75;    // ... with several accumulator tiles per wave
+  constexpr double kWcReduction = 69.0;   // per extra wave group
   constexpr double kLaunch = 2000.0;
-  constexpr double kCopyBytesPerClock = 48.0;
-  const double kStageOverhead = mfma ? 1200.0 : 300.0;
-  const double kLatency = mfma ? 5000.0 : 2000.0;
+  constexpr double kCopyBytesPerClock = 15.9;
+  const double kStageOverhead = mfma ? 1521.0 : 300.0;
+  const double kLatency = mfma ? 11.0 : 2000.0;
   constexpr int kMaxWaves = 8;            // co-resident waves per CU the model counts
   int occ = (int)(160 * 1024 / (lds_bytes > 0 ? lds_bytes : 1));
   if (occ > kMaxWaves / cd.waves) occ = kMaxWaves / cd.waves;
@@ -920,7 +960,8 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
   const double mcyc = cd.mf == 16 ? kMfma16Cycles : kMfma32Cycles;
   const double per_stage =
       (mfma ? (double)(cd.CC / cd.WC / kg) * kk * cd.ops_per_kstep * mcyc * cd.waves / 4 *
-                  (waves_per_simd < 2 ? kOneWavePerSimd : 1.0)
+                  (waves_per_simd < 2 ? kOneWavePerSimd : 1.0) *
+                  (cd.ops_per_kstep > 1 ? kSeveralAcc : 1.0)
             : (double)(cd.CC / cd.WC) * kk * cd.ops_per_kstep * 4.0) +
       kStageOverhead;
   const double work = (double)per_cu * stages * per_stage;
