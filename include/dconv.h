@@ -160,6 +160,33 @@ int dconv_multi_with_plan(const float *I, const float *F, float *O, int C, int M
                           int Wy, int K, const dconv_plan *plan, void *stream);
 
 /*
+ * dconv_plan_single_candidates -- every single-map plan for these sizes on a
+ * device with `num_cu` compute units (<= 0: 256), the input assumed 16-byte
+ * aligned with Wx a multiple of 4 (as dconv_plan_single_variant): each tile
+ * shape of the vector kernel (tall or short tiles, 64 or 16 lanes across a
+ * row) and, for DCONV_VARIANT_AUTO / _MFMA with K in 5..11, the matrix-core
+ * kernel, crossed with the division of the M filters into groups of
+ * workgroups (Section 3.1 divides the filters over processors, or the map).
+ * Fixed order; dconv_plan_single returns one of them.  Writes
+ * min(count, capacity) plans to `out` (may be NULL when capacity is 0) and
+ * the total to *count.
+ */
+int dconv_plan_single_candidates(int Wx, int Wy, int K, int M, int variant, int num_cu,
+                                 dconv_plan *out, int capacity, int *count);
+
+/*
+ * dconv_single_with_plan -- dconv_single with a plan chosen by the caller,
+ * which must equal (field by field) one of the candidates for these sizes on
+ * the current device and for the alignment of I (a 16-byte-aligned input
+ * with Wx a multiple of 4 has the candidates of
+ * dconv_plan_single_candidates; other inputs have the single-float staging
+ * kernel's); DCONV_EINVAL otherwise.  Semantics and returns as for
+ * dconv_single.
+ */
+int dconv_single_with_plan(const float *I, const float *F, float *O, int Wx, int Wy, int K,
+                           int M, const dconv_plan *plan, void *stream);
+
+/*
  * The paper's partition model (host arithmetic only, no device access).
  *
  * Section 2.2 and Table 1: to hide a global-memory latency of L clocks a
@@ -254,6 +281,22 @@ int dconv_model_multi(const dconv_device_params *dev, const dconv_latency_model 
  */
 int dconv_plan_multi_paper(int C, int M, int Wx, int Wy, int K, const dconv_device_params *dev,
                            dconv_plan *out);
+
+/*
+ * dconv_plan_single_paper -- the Section 3.1 division applied to this
+ * library's single-map plans for a device described by `dev`
+ * (dconv_model_single decides the method).  Method 1, filters divided over
+ * the processors and the map walked in P pieces: the vector-kernel candidate
+ * whose number of filter groups is closest to min(M, num_cu), then whose tile
+ * height is closest to Hout / P.  Method 2, the map divided over the
+ * processors and all filters applied by each: among the candidates with one
+ * filter group, the tile height closest to Hout / num_cu, then the most
+ * workgroups.  For comparison with the library's planner and with exhaustive
+ * search; `out` can be passed to dconv_single_with_plan when dev->num_cu is
+ * the device's count and the input is 16-byte aligned with Wx % 4 == 0.
+ */
+int dconv_plan_single_paper(int Wx, int Wy, int K, int M, const dconv_device_params *dev,
+                            dconv_plan *out);
 
 /*
  * dconv_probe_latency -- measure the latency the model above takes as input

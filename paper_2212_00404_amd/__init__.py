@@ -8,4 +8,5 @@ efficiency" (Section 2.1).  See ``dconv.py`` for the argument conventions and
 """
 from .dconv import (EXPORTED, GTX_1080TI, MI355X, Plan, load, model_latency,  # noqa: F401
                     model_multi, model_single, multi, plan_multi, plan_multi_candidates,
-                    plan_multi_paper, plan_single, probe_latency, single, strerror)
+                    plan_multi_paper, plan_single, plan_single_candidates, plan_single_paper,
+                    probe_latency, single, strerror)

@@ -21,6 +21,10 @@ CSRC = os.path.join(PKG, "csrc")
 INCLUDE = os.path.join(ROOT, "include")
 BUILD = os.path.join(ROOT, "_build")
 LIB = os.path.join(PKG, "libdconv.so")
+# Debug build with every kernel's LDS filled with NaN before first use
+# (-DDCONV_POISON_LDS): a GPU test runs it to catch reads of LDS that a
+# kernel did not write first.
+POISON_LIB = os.path.join(PKG, "libdconv_poison.so")
 PEAKS_SRC = os.path.join(PKG, "peaks", "peaks.hip")
 PEAKS_LIB = os.path.join(PKG, "libdconv_peaks.so")
 ARCH = "gfx950"
@@ -83,9 +87,9 @@ def _hipcc():
     return "hipcc"
 
 
-def _compile(src):
-    obj = os.path.join(BUILD, os.path.basename(src).replace(".hip", ".o"))
-    cmd = [_hipcc()] + CFLAGS + ["-c", src, "-o", obj]
+def _compile(src, out_dir=BUILD, extra=()):
+    obj = os.path.join(out_dir, os.path.basename(src).replace(".hip", ".o"))
+    cmd = [_hipcc()] + CFLAGS + list(extra) + ["-c", src, "-o", obj]
     res = subprocess.run(cmd, capture_output=True, text=True)
     noise = "'-packed-fp32-ops' is not a recognized feature"
     err = "\n".join(l for l in res.stderr.splitlines() if noise not in l)
@@ -104,21 +108,26 @@ def _link(objs, lib):
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source and link the library (and the peak
-    microbenchmarks, libdconv_peaks.so, from peaks/); returns the library's
-    path."""
-    os.makedirs(BUILD, exist_ok=True)
+    """Compile every source and link the library, its LDS-poisoning debug
+    twin (libdconv_poison.so) and the peak microbenchmarks
+    (libdconv_peaks.so, from peaks/); returns the library's path."""
+    poison_dir = os.path.join(BUILD, "poison")
+    os.makedirs(poison_dir, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
-    workers = min(len(srcs) + 1, max(1, min(8, os.cpu_count() or 1)))
+    jobs = ([(s, BUILD, ()) for s in srcs] + [(PEAKS_SRC, BUILD, ())] +
+            [(s, poison_dir, ("-DDCONV_POISON_LDS",)) for s in srcs])
+    workers = min(len(jobs), max(1, min(8, os.cpu_count() or 1)))
     with concurrent.futures.ThreadPoolExecutor(workers) as ex:
-        results = list(ex.map(_compile, srcs + [PEAKS_SRC]))
+        results = list(ex.map(lambda j: _compile(*j), jobs))
     if verbose:
         for obj, err in results:
             if err.strip():
                 print(err, file=sys.stderr)
     objs = [o for o, _ in results]
-    _link(objs[:-1], LIB)
-    _link(objs[-1:], PEAKS_LIB)
+    n = len(srcs)
+    _link(objs[:n], LIB)
+    _link(objs[n:n + 1], PEAKS_LIB)
+    _link(objs[n + 1:], POISON_LIB)
     return LIB
 
 

@@ -56,22 +56,13 @@ int validate_sizes(int C, int M, int Wx, int Wy, int K) {
   return DCONV_OK;
 }
 
-void export_single(const dconv::SinglePlan &p, dconv_plan *out) {
-  *out = dconv_plan{};
-  out->variant = p.kernel == 3 ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
-  out->kernel = p.kernel;
-  out->tile_m = p.m_per_block;
-  out->tile_h = p.tile_h;
-  out->tile_w = p.tile_w;
-  out->chunk_c = 1;
-  out->waves_c = 1;
-  out->grid_x = p.grid;
-  out->grid_y = p.grid_z;
-  out->grid_z = 1;
-  out->block = p.block;
-  out->lds_bytes = p.lds_bytes;
+// Whether two plans are the same, field by field.
+bool same_plan(const dconv_plan &a, const dconv_plan &b) {
+  return a.variant == b.variant && a.kernel == b.kernel && a.tile_m == b.tile_m &&
+         a.tile_h == b.tile_h && a.tile_w == b.tile_w && a.chunk_c == b.chunk_c &&
+         a.waves_c == b.waves_c && a.grid_x == b.grid_x && a.grid_y == b.grid_y &&
+         a.grid_z == b.grid_z && a.block == b.block && a.lds_bytes == b.lds_bytes;
 }
-
 
 }  // namespace
 
@@ -101,6 +92,49 @@ DCONV_EXPORT int dconv_single(const float *I, const float *F, float *O, int Wx, 
   return dconv_single_variant(I, F, O, Wx, Wy, K, M, DCONV_VARIANT_AUTO, stream);
 }
 
+DCONV_EXPORT int dconv_plan_single_candidates(int Wx, int Wy, int K, int M, int variant,
+                                              int num_cu, dconv_plan *out, int capacity,
+                                              int *count) {
+  if (!count || (capacity > 0 && !out)) return DCONV_ENULL;
+  if (capacity < 0) return DCONV_EINVAL;
+  if (variant != DCONV_VARIANT_AUTO && variant != DCONV_VARIANT_VALU &&
+      variant != DCONV_VARIANT_MFMA)
+    return DCONV_EINVAL;
+  int rc = validate_sizes(1, M, Wx, Wy, K);
+  if (rc != DCONV_OK) return rc;
+  std::vector<dconv::SinglePlan> all;
+  rc = dconv::single_candidates(Wx, Wy, K, M, num_cu > 0 ? num_cu : 256, true, variant, all);
+  *count = (int)all.size();
+  if (rc != DCONV_OK) return rc;
+  for (int i = 0; i < capacity && i < (int)all.size(); ++i)
+    dconv::export_single_plan(all[i], out + i);
+  return DCONV_OK;
+}
+
+DCONV_EXPORT int dconv_single_with_plan(const float *I, const float *F, float *O, int Wx, int Wy,
+                                        int K, int M, const dconv_plan *plan, void *stream) {
+  if (!I || !F || !O || !plan) return DCONV_ENULL;
+  int rc = validate_sizes(1, M, Wx, Wy, K);
+  if (rc != DCONV_OK) return rc;
+  int num_cu = 0;
+  if ((rc = current_num_cu(&num_cu)) != DCONV_OK) return rc;
+  std::vector<dconv::SinglePlan> all;
+  const bool aligned = (reinterpret_cast<uintptr_t>(I) & 15) == 0;
+  if (dconv::single_candidates(Wx, Wy, K, M, num_cu, aligned, DCONV_VARIANT_AUTO, all) !=
+      DCONV_OK)
+    return DCONV_EINVAL;
+  for (const auto &p : all) {
+    dconv_plan e;
+    dconv::export_single_plan(p, &e);
+    if (same_plan(e, *plan)) {
+      (void)hipGetLastError();  // report this launch only
+      const hipError_t err = dconv::launch_single(p, I, F, O, Wx, Wy, M, (hipStream_t)stream);
+      return err == hipSuccess ? DCONV_OK : DCONV_EHIP;
+    }
+  }
+  return DCONV_EINVAL;
+}
+
 namespace {
 
 // Launch a multi-channel plan.  A launch error still pending from earlier
@@ -113,12 +147,6 @@ int run_multi(const dconv::MultiPlan &p, const float *I, const float *F, float *
   return e == hipSuccess ? DCONV_OK : DCONV_EHIP;
 }
 
-bool same_plan(const dconv_plan &a, const dconv_plan &b) {
-  return a.variant == b.variant && a.kernel == b.kernel && a.tile_m == b.tile_m &&
-         a.tile_h == b.tile_h && a.tile_w == b.tile_w && a.chunk_c == b.chunk_c &&
-         a.waves_c == b.waves_c && a.grid_x == b.grid_x && a.grid_y == b.grid_y &&
-         a.grid_z == b.grid_z && a.block == b.block && a.lds_bytes == b.lds_bytes;
-}
 
 }  // namespace
 
@@ -204,7 +232,7 @@ DCONV_EXPORT int dconv_plan_single_variant(int Wx, int Wy, int K, int M, int var
   dconv::SinglePlan p;
   rc = dconv::plan_single(Wx, Wy, K, M, num_cu > 0 ? num_cu : 256, true, variant, &p);
   if (rc != DCONV_OK) return rc;
-  export_single(p, out);
+  dconv::export_single_plan(p, out);
   return DCONV_OK;
 }
 

@@ -11,6 +11,28 @@
 
 namespace dconv {
 
+// Debug builds (-DDCONV_POISON_LDS, libdconv_poison.so): every LDS buffer of
+// a kernel starts filled with NaN, so an output computed from LDS that the
+// kernel did not write first (a missing copy, wait or barrier before the
+// first use of a buffer) comes out non-finite.  Ordinary builds: nothing.
+#ifdef DCONV_POISON_LDS
+template <class T>
+__device__ __forceinline__ void poison_lds(T *p, int n) {
+  float *f = reinterpret_cast<float *>(p);
+  const int nf = n * (int)(sizeof(T) / sizeof(float));
+  for (int i = threadIdx.x; i < nf; i += blockDim.x) f[i] = __builtin_nanf("");
+}
+#define DCONV_POISON(...) \
+  do {                    \
+    __VA_ARGS__;          \
+    __syncthreads();      \
+  } while (0)
+#else
+#define DCONV_POISON(...) \
+  do {                    \
+  } while (0)
+#endif
+
 // ---------------------------------------------------------------------------
 // Single-map kernels (Eq. 2)
 // ---------------------------------------------------------------------------
@@ -37,8 +59,16 @@ constexpr int kMaxTiledK = 11;
 // or rows not 16-byte aligned).
 int plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, int variant,
                 SinglePlan *p);
+// Every single-map plan for these sizes (each tile shape of the family the
+// input's alignment allows, and the matrix-core kernel where it exists,
+// crossed with the division of the filters over workgroups), in a fixed
+// order; plan_single picks one of them.
+int single_candidates(int Wx, int Wy, int K, int M, int num_cu, bool aligned, int variant,
+                      std::vector<SinglePlan> &out);
 hipError_t launch_single(const SinglePlan &p, const float *I, const float *F, float *O,
                          int Wx, int Wy, int M, hipStream_t s);
+// The public description of a plan.
+void export_single_plan(const SinglePlan &p, dconv_plan *out);
 
 // ---------------------------------------------------------------------------
 // Multi-channel kernels (Eq. 1)

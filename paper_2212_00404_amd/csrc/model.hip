@@ -198,3 +198,57 @@ DCONV_EXPORT int dconv_plan_multi_paper(int C, int M, int Wx, int Wy, int K,
   dconv::export_multi_plan(all[best], out);
   return DCONV_OK;
 }
+
+// Section 3.1 applied to this library's single-map plans for a device
+// described by `dev`: the model's method decides how the work is divided.
+//   Method 1 (filters divided over the N processors, each walking the map in
+// P pieces along y): the vector-kernel candidate whose number of filter
+// groups is closest to min(M, N), then whose tile height is closest to a
+// P-th of the output rows.
+//   Method 2 (the map divided along y over the processors, every processor
+// applying all M filters, Q at a time): among the candidates that keep all
+// filters in one group, the one whose tile height is closest to an N-th of
+// the output rows, then the one with the most workgroups.
+DCONV_EXPORT int dconv_plan_single_paper(int Wx, int Wy, int K, int M,
+                                         const dconv_device_params *dev, dconv_plan *out) {
+  if (!dev || !out) return DCONV_ENULL;
+  if (!valid_device(dev)) return DCONV_EINVAL;
+  if (M < 1 || K < 1 || Wx < 1 || Wy < 1 || K > Wx || K > Wy) return DCONV_EINVAL;
+  dconv_latency_model lm;
+  int rc = dconv_model_latency(dev, &lm);
+  if (rc != DCONV_OK) return rc;
+  dconv_single_split sp;
+  if ((rc = dconv_model_single(dev, &lm, Wx, Wy, K, M, &sp)) != DCONV_OK) return rc;
+  std::vector<dconv::SinglePlan> all;
+  rc = dconv::single_candidates(Wx, Wy, K, M, dev->num_cu, true, DCONV_VARIANT_VALU, all);
+  if (rc != DCONV_OK) return rc;
+  const int64_t Hout = (int64_t)Wy - K + 1;
+  const int64_t N = dev->num_cu;
+  int best = -1;
+  auto dist = [](int64_t a, int64_t b) { return a > b ? a - b : b - a; };
+  for (int i = 0; i < (int)all.size(); ++i) {
+    const dconv::SinglePlan &p = all[i];
+    if (best < 0) {
+      best = i;
+      continue;
+    }
+    const dconv::SinglePlan &b = all[best];
+    if (sp.method == 1) {
+      const int64_t groups = std::min<int64_t>(M, N);
+      const int64_t rows = ceil_div64(Hout, sp.P);
+      const int64_t dg = dist(p.grid_z, groups), dgb = dist(b.grid_z, groups);
+      const int64_t dr = dist(p.tile_h, rows), drb = dist(b.tile_h, rows);
+      if (dg < dgb || (dg == dgb && (dr < drb || (dr == drb && p.tile_w > b.tile_w)))) best = i;
+    } else {
+      const int64_t rows = ceil_div64(Hout, N);
+      const bool one = p.grid_z == 1, oneb = b.grid_z == 1;
+      const int64_t dr = dist(p.tile_h, rows), drb = dist(b.tile_h, rows);
+      if ((one && !oneb) ||
+          (one == oneb && (dr < drb || (dr == drb && (int64_t)p.grid * p.grid_z >
+                                                         (int64_t)b.grid * b.grid_z))))
+        best = i;
+    }
+  }
+  dconv::export_single_plan(all[best], out);
+  return DCONV_OK;
+}

@@ -268,6 +268,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   constexpr bool PAIR = Cfg::PAIR;
   __shared__ float buf0[Cfg::BUF0];
   __shared__ float buf1[Cfg::BUF];
+  DCONV_POISON(poison_lds(buf0, Cfg::BUF0), poison_lds(buf1, Cfg::BUF));
 
   int tile, mt;
   block_coords(a, tile, mt);

@@ -271,6 +271,7 @@ __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_ti
     int Wx, int Wy, int M, int tiles_x, int ntiles, int m_per_block) {
   using S = TileShape<K, R, L>;
   __shared__ float4 tile[S::IH * S::IW4];
+  DCONV_POISON(poison_lds(tile, S::IH * S::IW4));
 
   const int Hout = Wy - K + 1;
   const int Wout = Wx - K + 1;
@@ -435,6 +436,8 @@ __global__ __launch_bounds__(kBlock, (MfmaOcc<K>::value)) void single_mfma(
   __shared__ float4 tile0[S::BUF4];
   __shared__ float4 tile1[S::BUF4];
   __shared__ float band[4 * K * NT];
+  DCONV_POISON(poison_lds(tile0, S::BUF4), poison_lds(tile1, S::BUF4),
+               poison_lds(band, 4 * K * NT));
 
   const int Hout = Wy - K + 1;
   const int Wout = Wx - K + 1;
@@ -569,9 +572,10 @@ __global__ __launch_bounds__(256) void single_generic(
 
 // Persistent workgroups: as many as fit on the chip at once.  Filters reuse
 // the staged tile; they are split over workgroups only as far as needed to
-// fill the chip when there are fewer tiles than slots.
+// fill the chip when there are fewer tiles than slots (or into `force_splits`
+// groups when that is given, for the candidate plans).
 void plan_persistent(int Wx, int Wy, int K, int M, int num_cu, int th, int tw, int occupancy,
-                     SinglePlan *p) {
+                     SinglePlan *p, int force_splits = 0) {
   const int Hout = Wy - K + 1, Wout = Wx - K + 1;
   p->tile_h = th;
   p->tile_w = tw;
@@ -579,7 +583,7 @@ void plan_persistent(int Wx, int Wy, int K, int M, int num_cu, int th, int tw, i
   p->tiles_y = (Hout + th - 1) / th;
   const int ntiles = p->tiles_x * p->tiles_y;
   const int slots = occupancy * num_cu;
-  int splits = (slots + ntiles - 1) / ntiles;
+  int splits = force_splits > 0 ? force_splits : (slots + ntiles - 1) / ntiles;
   if (splits > M) splits = M;
   if (splits < 1) splits = 1;
   p->m_per_block = (M + splits - 1) / splits;
@@ -747,6 +751,130 @@ int plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, int vari
   p->block = 256;
   p->lds_bytes = 0;
   return DCONV_OK;
+}
+
+namespace {
+
+// The filter divisions tried for one tile shape: 1, 2, 4, ... groups up to
+// M, M itself, and the planner's own (enough groups to fill the chip).
+void add_splits(int Wx, int Wy, int K, int M, int num_cu, int occupancy, const SinglePlan &base,
+                std::vector<SinglePlan> &out) {
+  const int Hout = Wy - K + 1, Wout = Wx - K + 1;
+  const int ntiles = ((Wout + base.tile_w - 1) / base.tile_w) * ((Hout + base.tile_h - 1) / base.tile_h);
+  const int slots = occupancy * num_cu;
+  std::vector<int> splits;
+  for (int s = 1; s < M; s *= 2) splits.push_back(s);
+  splits.push_back(M);
+  splits.push_back((slots + ntiles - 1) / ntiles);
+  const size_t first = out.size();
+  for (int s : splits) {
+    SinglePlan p = base;
+    plan_persistent(Wx, Wy, K, M, num_cu, base.tile_h, base.tile_w, occupancy, &p, s);
+    bool dup = false;
+    for (size_t i = first; i < out.size(); ++i)
+      dup = dup || (out[i].m_per_block == p.m_per_block && out[i].grid == p.grid &&
+                    out[i].grid_z == p.grid_z);
+    if (!dup) out.push_back(p);
+  }
+}
+
+template <int K, bool VEC4>
+void tiled_candidates(int Wx, int Wy, int M, int num_cu, std::vector<SinglePlan> &out) {
+  constexpr int RA = Rows<K, VEC4>::value;
+  constexpr int OCC = Occupancy<K, VEC4>::value;
+  SinglePlan b{};
+  b.kernel = VEC4 ? 0 : 2;
+  b.K = K;
+  b.block = kBlock;
+  // tall (or the only) tiles
+  b.rows = RA;
+  b.lanes = kLanes;
+  b.tile_h = TileShape<K, RA>::TH;
+  b.tile_w = TileShape<K, RA>::TW;
+  b.lds_bytes = TileShape<K, RA>::LDS;
+  add_splits(Wx, Wy, K, M, num_cu, OCC, b, out);
+  if constexpr (RA > kShortRows) {
+    b.rows = kShortRows;
+    b.tile_h = TileShape<K, kShortRows>::TH;
+    b.tile_w = TileShape<K, kShortRows>::TW;
+    b.lds_bytes = TileShape<K, kShortRows>::LDS;
+    add_splits(Wx, Wy, K, M, num_cu, OCC, b, out);
+  }
+  if constexpr (VEC4 && K <= kNarrowMaxK) {
+    using SN = TileShape<K, RA, kNarrowLanes>;
+    b.rows = RA;
+    b.lanes = kNarrowLanes;
+    b.tile_h = SN::TH;
+    b.tile_w = SN::TW;
+    b.lds_bytes = SN::LDS;
+    add_splits(Wx, Wy, K, M, num_cu, OCC, b, out);
+  }
+}
+
+template <int K>
+void mfma_candidates(int Wx, int Wy, int M, int num_cu, std::vector<SinglePlan> &out) {
+  using S = MfmaTileShape<K>;
+  SinglePlan b{};
+  b.kernel = 3;
+  b.K = K;
+  b.rows = 8;
+  b.lanes = kLanes;
+  b.block = kBlock;
+  b.tile_h = S::TH;
+  b.tile_w = kTileW;
+  b.lds_bytes = S::LDS;
+  add_splits(Wx, Wy, K, M, num_cu, MfmaOcc<K>::value, b, out);
+}
+
+}  // namespace
+
+int single_candidates(int Wx, int Wy, int K, int M, int num_cu, bool aligned, int variant,
+                      std::vector<SinglePlan> &out) {
+  out.clear();
+  if (num_cu <= 0) num_cu = 256;
+  const bool vec4 = aligned && (Wx % 4 == 0);
+  const bool valu = variant != DCONV_VARIANT_MFMA;
+  const bool mfma = variant != DCONV_VARIANT_VALU && vec4 && K >= kMfmaMinK && K <= kMaxTiledK;
+  if (K > kMaxTiledK) {
+    if (!valu) return DCONV_EUNSUPPORTED;
+    SinglePlan p;
+    plan_single(Wx, Wy, K, M, num_cu, aligned, DCONV_VARIANT_VALU, &p);
+    out.push_back(p);
+    return DCONV_OK;
+  }
+  switch (K) {
+#define DCONV_CANDIDATES_K(k)                                                    \
+  case k:                                                                        \
+    if (valu) {                                                                  \
+      if (vec4) tiled_candidates<k, true>(Wx, Wy, M, num_cu, out);               \
+      else tiled_candidates<k, false>(Wx, Wy, M, num_cu, out);                   \
+    }                                                                            \
+    if (mfma) mfma_candidates<(k >= kMfmaMinK ? k : kMfmaMinK)>(Wx, Wy, M, num_cu, out); \
+    break;
+    DCONV_CANDIDATES_K(1) DCONV_CANDIDATES_K(2) DCONV_CANDIDATES_K(3) DCONV_CANDIDATES_K(4)
+    DCONV_CANDIDATES_K(5) DCONV_CANDIDATES_K(6) DCONV_CANDIDATES_K(7) DCONV_CANDIDATES_K(8)
+    DCONV_CANDIDATES_K(9) DCONV_CANDIDATES_K(10) DCONV_CANDIDATES_K(11)
+#undef DCONV_CANDIDATES_K
+    default:
+      break;
+  }
+  return out.empty() ? DCONV_EUNSUPPORTED : DCONV_OK;
+}
+
+void export_single_plan(const SinglePlan &p, dconv_plan *out) {
+  *out = dconv_plan{};
+  out->variant = p.kernel == 3 ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
+  out->kernel = p.kernel;
+  out->tile_m = p.m_per_block;
+  out->tile_h = p.tile_h;
+  out->tile_w = p.tile_w;
+  out->chunk_c = 1;
+  out->waves_c = 1;
+  out->grid_x = p.grid;
+  out->grid_y = p.grid_z;
+  out->grid_z = 1;
+  out->block = p.block;
+  out->lds_bytes = p.lds_bytes;
 }
 
 hipError_t launch_single(const SinglePlan &p, const float *I, const float *F, float *O,

@@ -32,9 +32,11 @@ VARIANT_MFMA = 2
 _VARIANTS = {"auto": VARIANT_AUTO, "valu": VARIANT_VALU, "mfma": VARIANT_MFMA}
 
 EXPORTED = ("dconv_single", "dconv_single_variant", "dconv_multi", "dconv_multi_variant",
-            "dconv_strerror", "dconv_plan_single", "dconv_plan_single_variant", "dconv_plan_multi", "dconv_plan_multi_candidates",
-            "dconv_multi_with_plan", "dconv_model_latency", "dconv_model_single",
-            "dconv_model_multi", "dconv_plan_multi_paper", "dconv_probe_latency")
+            "dconv_strerror", "dconv_plan_single", "dconv_plan_single_variant",
+            "dconv_plan_single_candidates", "dconv_single_with_plan", "dconv_plan_multi",
+            "dconv_plan_multi_candidates", "dconv_multi_with_plan", "dconv_model_latency",
+            "dconv_model_single", "dconv_model_multi", "dconv_plan_multi_paper",
+            "dconv_plan_single_paper", "dconv_probe_latency")
 
 
 class Plan(ctypes.Structure):
@@ -126,6 +128,11 @@ def load(path: str | None = None):
     lib.dconv_single_variant.restype = i
     lib.dconv_plan_single_variant.argtypes = [i, i, i, i, i, i, ctypes.POINTER(Plan)]
     lib.dconv_plan_single_variant.restype = i
+    lib.dconv_plan_single_candidates.argtypes = [i, i, i, i, i, i, ctypes.POINTER(Plan), i,
+                                                 ctypes.POINTER(i)]
+    lib.dconv_plan_single_candidates.restype = i
+    lib.dconv_single_with_plan.argtypes = [vp, vp, vp, i, i, i, i, ctypes.POINTER(Plan), vp]
+    lib.dconv_single_with_plan.restype = i
     lib.dconv_multi.argtypes = [vp, vp, vp, i, i, i, i, i, vp]
     lib.dconv_multi.restype = i
     lib.dconv_multi_variant.argtypes = [vp, vp, vp, i, i, i, i, i, i, vp]
@@ -150,6 +157,8 @@ def load(path: str | None = None):
     lib.dconv_model_multi.restype = i
     lib.dconv_plan_multi_paper.argtypes = [i, i, i, i, i, dp, ctypes.POINTER(Plan)]
     lib.dconv_plan_multi_paper.restype = i
+    lib.dconv_plan_single_paper.argtypes = [i, i, i, i, dp, ctypes.POINTER(Plan)]
+    lib.dconv_plan_single_paper.restype = i
     lib.dconv_probe_latency.argtypes = [vp, i, vp, vp]
     lib.dconv_probe_latency.restype = i
     if path is None:
@@ -203,10 +212,12 @@ class _OnDevice:
 
 
 def single(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None,
-           variant: str = "auto") -> torch.Tensor:
+           variant: str = "auto", plan: dict | None = None) -> torch.Tensor:
     """Eq. 2: ``I[Wy, Wx]``, ``F[M, K, K]`` -> ``O[M, Wy-K+1, Wx-K+1]`` (fp32).
 
     ``variant`` forces the kernel family: ``"auto"``, ``"valu"`` or ``"mfma"``.
+    ``plan``: one of ``plan_single_candidates(...)`` for these sizes
+    (overrides ``variant``).
     """
     _require(I, "I", 2)
     _require(F, "F", 3)
@@ -228,8 +239,12 @@ def single(I: torch.Tensor, F: torch.Tensor, out: torch.Tensor | None = None,
         if tuple(out.shape) != shape or out.device != I.device:
             raise ValueError("out must be %r on %s" % (shape, I.device))
     with _OnDevice(I.device):
-        rc = load().dconv_single_variant(I.data_ptr(), F.data_ptr(), out.data_ptr(), Wx, Wy, K,
-                                         M, _VARIANTS[variant], _stream(I.device))
+        if plan is not None:
+            rc = load().dconv_single_with_plan(I.data_ptr(), F.data_ptr(), out.data_ptr(), Wx, Wy,
+                                               K, M, ctypes.byref(Plan(**plan)), _stream(I.device))
+        else:
+            rc = load().dconv_single_variant(I.data_ptr(), F.data_ptr(), out.data_ptr(), Wx, Wy,
+                                             K, M, _VARIANTS[variant], _stream(I.device))
     _check(rc)
     return out
 
@@ -279,6 +294,28 @@ def plan_single(Wx: int, Wy: int, K: int, M: int, num_cu: int = 256,
     p = Plan()
     _check(load().dconv_plan_single_variant(Wx, Wy, K, M, _VARIANTS[variant], num_cu,
                                             ctypes.byref(p)))
+    return p.as_dict()
+
+
+def plan_single_candidates(Wx: int, Wy: int, K: int, M: int, variant: str = "auto",
+                           num_cu: int = 256) -> list:
+    """Every plan ``dconv_single_with_plan`` accepts for these sizes (a
+    16-byte-aligned input with Wx % 4 == 0; host logic)."""
+    n = ctypes.c_int(0)
+    lib = load()
+    _check(lib.dconv_plan_single_candidates(Wx, Wy, K, M, _VARIANTS[variant], num_cu, None, 0,
+                                            ctypes.byref(n)))
+    arr = (Plan * max(n.value, 1))()
+    _check(lib.dconv_plan_single_candidates(Wx, Wy, K, M, _VARIANTS[variant], num_cu, arr,
+                                            n.value, ctypes.byref(n)))
+    return [arr[k].as_dict() for k in range(n.value)]
+
+
+def plan_single_paper(Wx: int, Wy: int, K: int, M: int, dev: dict) -> dict:
+    """The single-map candidate the Section 3.1 division picks for a device."""
+    p = Plan()
+    _check(load().dconv_plan_single_paper(Wx, Wy, K, M, ctypes.byref(_device(dev)),
+                                          ctypes.byref(p)))
     return p.as_dict()
 
 

@@ -9,7 +9,7 @@ import torch
 
 import paper_2212_00404_amd as dc
 from dconv_workloads import random_arrays
-from gpu_util import assert_exact, oracle_multi
+from gpu_util import assert_exact, oracle_multi, oracle_single
 
 pytestmark = pytest.mark.gpu
 
@@ -69,3 +69,38 @@ def test_latency_probe_orders_the_hierarchy():
     for r in (small, mid, large):
         assert r["cycles_per_load"] > 20 and r["ns_per_load"] > 10
     assert small["ns_per_load"] < mid["ns_per_load"] < large["ns_per_load"]
+
+
+# (Wx, Wy, K, M): single-map layers whose candidates cover tall and short
+# tiles, 16-lane narrow rows, the matrix-core kernel, and filter divisions
+# from one group to one filter per group
+SINGLE_LAYERS = [(40, 36, 3, 12), (70, 33, 5, 9), (132, 61, 7, 5), (64, 64, 11, 3), (300, 20, 1, 6),
+                 (96, 50, 9, 4), (28, 28, 3, 40)]
+
+
+@pytest.mark.parametrize("layer", SINGLE_LAYERS, ids=[str(l) for l in SINGLE_LAYERS])
+def test_every_single_candidate_plan_is_exact(layer):
+    Wx, Wy, K, M = layer
+    I, F = random_arrays(1, M, Wx, Wy, K, seed=sum(layer) * 17 + 3, variant="int")
+    I, F = I[0], F[:, 0]
+    O64, _ = oracle_single(I, F)
+    It, Ft = torch.from_numpy(I).cuda(), torch.from_numpy(F).cuda()
+    cands = dc.plan_single_candidates(Wx, Wy, K, M)
+    assert len(cands) >= 2
+    assert dc.plan_single(Wx, Wy, K, M) in cands
+    assert dc.plan_single_paper(Wx, Wy, K, M, dc.MI355X) in cands
+    outs = [dc.single(It, Ft, plan=p) for p in cands]
+    torch.cuda.synchronize()
+    for p, o in zip(cands, outs):
+        assert_exact(o.cpu().numpy(), O64, "%r plan %r" % (layer, p))
+
+
+def test_foreign_single_plan_is_rejected():
+    Wx, Wy, K, M = 64, 40, 3, 4
+    I, F = random_arrays(1, M, Wx, Wy, K, seed=2)
+    It, Ft = torch.from_numpy(I[0]).cuda(), torch.from_numpy(F[:, 0]).cuda()
+    p = dict(dc.plan_single(Wx, Wy, K, M))
+    for field, delta in (("grid_x", 1), ("tile_m", 1), ("kernel", 1), ("tile_h", 4)):
+        bad = dict(p, **{field: p[field] + delta})
+        with pytest.raises(RuntimeError, match="invalid"):
+            dc.single(It, Ft, plan=bad)

@@ -188,3 +188,57 @@ def test_paper_rule_plan(layer):
         assert p["tile_h"] * p["tile_w"] == max(c["tile_h"] * c["tile_w"] for c in same_m)
     else:
         assert work(p) == max(work(c) for c in unsplit)
+
+
+SINGLE_LAYERS = [(4096, 4096, 3, 1), (4096, 4096, 11, 1), (28, 28, 3, 512), (56, 56, 5, 256),
+                 (112, 112, 3, 128), (224, 224, 5, 64), (512, 512, 1, 128), (1024, 1024, 3, 32),
+                 (64, 64, 3, 1), (300, 70, 7, 9), (4097, 100, 9, 3)]
+
+
+@pytest.mark.parametrize("layer", SINGLE_LAYERS, ids=[str(l) for l in SINGLE_LAYERS])
+def test_single_candidates(layer):
+    """Every single-map candidate covers the output and the filters, fits
+    the LDS, and the planner's and the paper rule's plans are among them."""
+    Wx, Wy, K, M = layer
+    cands = dc.plan_single_candidates(Wx, Wy, K, M)
+    assert cands
+    assert dc.plan_single(Wx, Wy, K, M) in cands
+    assert dc.plan_single_paper(Wx, Wy, K, M, dc.MI355X) in cands
+    Hout, Wout = Wy - K + 1, Wx - K + 1
+    seen = set()
+    for p in cands:
+        key = (p["kernel"], p["tile_h"], p["tile_w"], p["tile_m"], p["grid_x"], p["grid_y"])
+        assert key not in seen
+        seen.add(key)
+        assert p["lds_bytes"] <= 160 * 1024
+        if p["kernel"] == 1:
+            assert p["grid_x"] * p["block"] >= M * Hout * Wout
+            continue
+        tiles = -(-Hout // p["tile_h"]) * -(-Wout // p["tile_w"])
+        assert 1 <= p["grid_x"] <= tiles
+        assert p["grid_y"] * p["tile_m"] >= M > (p["grid_y"] - 1) * p["tile_m"]
+    for v in ("valu", "mfma"):
+        if v == "mfma" and not (5 <= K <= 11 and Wx % 4 == 0):
+            continue
+        sub = dc.plan_single_candidates(Wx, Wy, K, M, v)
+        assert all(p in cands for p in sub)
+        assert all(p["variant"] == (2 if v == "mfma" else 1) for p in sub)
+
+
+@pytest.mark.parametrize("layer", SINGLE_LAYERS, ids=[str(l) for l in SINGLE_LAYERS])
+def test_single_paper_rule_plan(layer):
+    """The Section 3.1 rule: method 1 takes the vector candidate whose filter
+    groups are closest to min(M, N); method 2 keeps all filters in one group
+    where a candidate does."""
+    Wx, Wy, K, M = layer
+    dev = dc.MI355X
+    p = dc.plan_single_paper(Wx, Wy, K, M, dev)
+    split = dc.model_single(dev, Wx, Wy, K, M)
+    vec = dc.plan_single_candidates(Wx, Wy, K, M, "valu")
+    assert p in vec
+    if split["method"] == 1:
+        target = min(M, dev["num_cu"])
+        assert abs(p["grid_y"] - target) == min(abs(c["grid_y"] - target) for c in vec)
+    else:
+        if any(c["grid_y"] == 1 for c in vec):
+            assert p["grid_y"] == 1
