@@ -75,6 +75,48 @@ int main(void) {
     check(dconv_model_latency(NULL, &m) == DCONV_ENULL, "latency model NULL");
   }
 
+  {
+    /* The host planners over a sweep of shapes (under the sanitizer build
+     * this walks every planning path): every candidate list, the planners'
+     * choices and the paper-rule plans, which must be among the candidates. */
+    static const int Ks[] = {1, 2, 3, 5, 7, 9, 11, 13};
+    static const int Ws[] = {1, 7, 9, 16, 30, 61, 114, 257, 1030};
+    static const int Ms[] = {1, 3, 64, 130, 512};
+    static const int Cs[] = {1, 5, 64, 513};
+    dconv_device_params mi = {900.0, 8000.0, 2400.0, 256, 64, 2, 32, 4, 160 * 1024};
+    dconv_plan cand[256], p, pp;
+    size_t a, b, c, d;
+    mi.wave_size = 64;
+    for (a = 0; a < sizeof(Ks) / sizeof(Ks[0]); ++a)
+      for (b = 0; b < sizeof(Ws) / sizeof(Ws[0]); ++b)
+        for (c = 0; c < sizeof(Ms) / sizeof(Ms[0]); ++c) {
+          const int K = Ks[a], W = Ws[b], M = Ms[c];
+          int n = 0, i, found = 0;
+          if (K > W) continue;
+          check(dconv_plan_single_candidates(W, W + 3, K, M, DCONV_VARIANT_AUTO, 256, cand, 256,
+                                             &n) == DCONV_OK && n >= 1 && n <= 256,
+                "single candidates");
+          check(dconv_plan_single(W, W + 3, K, M, 256, &p) == DCONV_OK, "plan single (sweep)");
+          for (i = 0; i < n; ++i) found |= memcmp(&cand[i], &p, sizeof p) == 0;
+          check(found, "the single planner's plan is a candidate");
+          check(dconv_plan_single_paper(W, W + 3, K, M, &mi, &pp) == DCONV_OK, "single paper plan");
+          for (d = 0; d < sizeof(Cs) / sizeof(Cs[0]); ++d) {
+            const int C = Cs[d];
+            int v;
+            for (v = DCONV_VARIANT_AUTO; v <= DCONV_VARIANT_MFMA; ++v) {
+              const int rc = dconv_plan_multi(C, M, W + 2, W, K, v, 256, &p);
+              check(rc == DCONV_OK || (v == DCONV_VARIANT_MFMA && rc == DCONV_EUNSUPPORTED),
+                    "plan multi (sweep)");
+            }
+            check(dconv_plan_multi_candidates(C, M, W + 2, W, K, DCONV_VARIANT_AUTO, 256, cand, 256,
+                                              &n) == DCONV_OK && n >= 1,
+                  "multi candidates");
+            check(dconv_plan_multi_paper(C, M, W + 2, W, K, &mi, &pp) == DCONV_OK,
+                  "multi paper plan");
+          }
+        }
+  }
+
   if (failures == 0) printf("ok\n");
   return failures == 0 ? 0 : 1;
 }
