@@ -85,8 +85,8 @@ WORKLOADS = {w.name: w for w in [
     _multi("multi_c64_114x114_m128_k3", 64, 114, 128, 3),
     _multi("multi_c128_60x60_m128_k5", 128, 60, 128, 5),
     _multi("multi_c256_28x28_m256_k1", 256, 28, 256, 1),
-    # filters larger than the matrix-core kernels take (K > 7): the vector
-    # family's layers
+    # large filters (K = 9, 11) on small maps: long inner products per
+    # output, few output tiles
     _multi("multi_c64_40x40_m64_k9", 64, 40, 64, 9),
     _multi("multi_c32_42x42_m64_k11", 32, 42, 64, 11),
     # one input map, many filters: the single-channel layers the paper

@@ -100,7 +100,7 @@ int dconv_multi(const float *I, const float *F, float *O, int C, int M, int Wx,
  * dconv_multi_variant -- dconv_multi with the kernel family forced
  * (DCONV_VARIANT_AUTO, _VALU or _MFMA), for A/B measurement of the vector
  * and matrix-core paths.  DCONV_EUNSUPPORTED if the forced family has no
- * kernel for this K (the matrix-core family covers K <= 7).
+ * kernel for this K (the matrix-core family covers K <= 11).
  */
 int dconv_multi_variant(const float *I, const float *F, float *O, int C, int M,
                         int Wx, int Wy, int K, int variant, void *stream);

@@ -833,7 +833,7 @@ hipError_t launch_valu_k(const MultiPlan &p, const float *I, const float *F, flo
 // ---------------------------------------------------------------------------
 // Planner
 // ---------------------------------------------------------------------------
-constexpr int kMfmaMaxK = 7;
+constexpr int kMfmaMaxK = 11;
 constexpr int kGenericKernel = 99;
 
 struct TileChoice { int tpy, tpx, tiles_x, tiles_y; int64_t lanes; };
@@ -875,6 +875,10 @@ int shape_lds_bytes(int K) {
     case 5: return ShapeCfg<5, S>::LDS_BYTES;
     case 6: return ShapeCfg<6, S>::LDS_BYTES;
     case 7: return ShapeCfg<7, S>::LDS_BYTES;
+    case 8: return ShapeCfg<8, S>::LDS_BYTES;
+    case 9: return ShapeCfg<9, S>::LDS_BYTES;
+    case 10: return ShapeCfg<10, S>::LDS_BYTES;
+    case 11: return ShapeCfg<11, S>::LDS_BYTES;
     default: return INT32_MAX;
   }
 }
@@ -889,6 +893,10 @@ int shape_cc(int K) {
     case 5: return ShapeCfg<5, S>::CC;
     case 6: return ShapeCfg<6, S>::CC;
     case 7: return ShapeCfg<7, S>::CC;
+    case 8: return ShapeCfg<8, S>::CC;
+    case 9: return ShapeCfg<9, S>::CC;
+    case 10: return ShapeCfg<10, S>::CC;
+    case 11: return ShapeCfg<11, S>::CC;
     default: return 0;
   }
 }
@@ -1118,6 +1126,10 @@ hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, floa
       case 5: return launch_mfma_k<5>(p, I, F, O, a, st);
       case 6: return launch_mfma_k<6>(p, I, F, O, a, st);
       case 7: return launch_mfma_k<7>(p, I, F, O, a, st);
+      case 8: return launch_mfma_k<8>(p, I, F, O, a, st);
+      case 9: return launch_mfma_k<9>(p, I, F, O, a, st);
+      case 10: return launch_mfma_k<10>(p, I, F, O, a, st);
+      case 11: return launch_mfma_k<11>(p, I, F, O, a, st);
       default: return hipErrorInvalidValue;
     }
   }

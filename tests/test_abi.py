@@ -156,11 +156,11 @@ def test_plans_for_workloads(name):
         if w.Wx >= 1024:
             assert p["grid_x"] * p["grid_y"] >= 256
     else:
-        for v in ("auto", "valu") + (("mfma",) if w.K <= 7 else ()):
+        for v in ("auto", "valu") + (("mfma",) if w.K <= 11 else ()):
             _check_multi_plan(w.C, w.M, w.Wx, w.Wy, w.K, v)
         p = dc.plan_multi(w.C, w.M, w.Wx, w.Wy, w.K)
-        # the matrix cores wherever a kernel exists (K <= 7)
-        assert p["variant"] == (dc.dconv.VARIANT_MFMA if w.K <= 7 else dc.dconv.VARIANT_VALU)
+        # the matrix cores wherever a kernel exists (K <= 11)
+        assert p["variant"] == (dc.dconv.VARIANT_MFMA if w.K <= 11 else dc.dconv.VARIANT_VALU)
 
 
 @pytest.mark.parametrize("shape", [
@@ -192,13 +192,13 @@ def test_single_auto_uses_the_vector_kernel():
     (16, 16, 64, 64, 31), (64, 130, 57, 31, 7), (3, 64, 224, 224, 7), (1, 1, 4096, 2, 2)])
 def test_multi_plan_shapes(shape):
     C, M, Wx, Wy, K = shape
-    for v in ("auto", "valu") + (("mfma",) if K <= 7 else ()):
+    for v in ("auto", "valu") + (("mfma",) if K <= 11 else ()):
         _check_multi_plan(C, M, Wx, Wy, K, v)
 
 
 def test_mfma_refuses_large_filters():
     with pytest.raises(RuntimeError):
-        dc.plan_multi(4, 4, 20, 20, 9, "mfma")
+        dc.plan_multi(4, 4, 20, 20, 12, "mfma")
 
 
 def test_wave_split_test_shapes_split_inside_the_workgroup():
@@ -228,7 +228,7 @@ def test_single_plan_random(shape):
 
 @pytest.mark.parametrize("shape", MULTI_RANDOM, ids=[str(s) for s in MULTI_RANDOM])
 def test_multi_plan_random(shape):
-    for v in ("auto", "valu") + (("mfma",) if shape[4] <= 7 else ()):
+    for v in ("auto", "valu") + (("mfma",) if shape[4] <= 11 else ()):
         _check_multi_plan(*shape, variant=v)
 
 

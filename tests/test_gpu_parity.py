@@ -47,7 +47,7 @@ def test_single_workload(name, variant):
 @pytest.mark.parametrize("variant", ["float", "int"])
 def test_multi_workload(name, family, variant):
     I, F = make(name, variant)
-    if family == "mfma" and WORKLOADS[name].K > 7:
+    if family == "mfma" and WORKLOADS[name].K > 11:
         with pytest.raises(RuntimeError, match="cannot run"):
             gpu_multi(I, F, family)
         return
@@ -114,7 +114,7 @@ MULTI_SHAPES = [
 @pytest.mark.parametrize("shape", MULTI_SHAPES, ids=[str(s) for s in MULTI_SHAPES])
 def test_multi_shapes(shape):
     C, M, Wx, Wy, K = shape
-    families = ["auto", "valu"] + (["mfma"] if K <= 7 else [])
+    families = ["auto", "valu"] + (["mfma"] if K <= 11 else [])
     I, F = random_arrays(C, M, Wx, Wy, K, seed=sum(shape) * 104729)
     O64, A64 = oracle_multi(I, F)
     Ii, Fi = random_arrays(C, M, Wx, Wy, K, seed=sum(shape) * 104729 + 1, variant="int")
@@ -340,7 +340,7 @@ def test_misaligned_base_pointers(offsets):
         O64, _ = oracle_multi(I, F)
         _, It = _offset_view(I, oi, dev)
         _, Ft = _offset_view(F, of, dev)
-        for fam in ["auto", "valu"] + (["mfma"] if K <= 7 else []):
+        for fam in ["auto", "valu"] + (["mfma"] if K <= 11 else []):
             flat, Ot = _offset_view(np.zeros(O64.shape, np.float32), oo, dev)
             dc.multi(It, Ft, out=Ot, variant=fam)
             torch.cuda.synchronize()

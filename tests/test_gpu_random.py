@@ -32,7 +32,7 @@ def test_single_random(shape):
 @pytest.mark.parametrize("shape", MULTI_RANDOM, ids=[str(s) for s in MULTI_RANDOM])
 def test_multi_random(shape):
     C, M, Wx, Wy, K = shape
-    fams = ["auto", "valu"] + (["mfma"] if K <= 7 else [])
+    fams = ["auto", "valu"] + (["mfma"] if K <= 11 else [])
     I, F = random_arrays(C, M, Wx, Wy, K, seed=hash(shape) % 2**31)
     Ii, Fi = random_arrays(C, M, Wx, Wy, K, seed=hash(shape) % 2**31 + 1, variant="int")
     O64, A64 = oracle_multi(I, F)

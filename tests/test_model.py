@@ -142,7 +142,7 @@ def test_candidates_cover_the_planner_and_fit(layer):
     assert cands
     assert dc.plan_multi(C, M, Wx, Wy, K) in cands
     for v in ("valu", "mfma"):
-        if v == "mfma" and K > 7:
+        if v == "mfma" and K > 11:
             continue
         sub = dc.plan_multi_candidates(C, M, Wx, Wy, K, v)
         assert dc.plan_multi(C, M, Wx, Wy, K, v) in sub
