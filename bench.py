@@ -41,7 +41,8 @@ SWEEPS = (DEFAULT_STEP, SWEEP, "single_multi_filter", "multi_layers", "paper_mul
 # Sources each kernel family is built from: recorded HBM traffic stays valid
 # while these are unchanged.
 SINGLE_SOURCES = ("single.hip", "xcd.h")
-MULTI_SOURCES = ("multi.hip", "xcd.h")
+MULTI_SOURCES = ("multi.hip", "multi_kernels.h", "multi_mfma_k1_3.hip", "multi_mfma_k4_6.hip",
+                 "multi_mfma_k7_9.hip", "multi_mfma_k10_11.hip", "xcd.h")
 
 
 def parse():

@@ -117,8 +117,11 @@ def build(verbose: bool = False) -> str:
     jobs = ([(s, BUILD, ()) for s in srcs] + [(PEAKS_SRC, BUILD, ())] +
             [(s, poison_dir, ("-DDCONV_POISON_LDS",)) for s in srcs])
     workers = min(len(jobs), max(1, min(8, os.cpu_count() or 1)))
+    # the matrix-core kernel units take longest: start them first
+    order = sorted(range(len(jobs)), key=lambda i: "multi_mfma" not in jobs[i][0])
     with concurrent.futures.ThreadPoolExecutor(workers) as ex:
-        results = list(ex.map(lambda j: _compile(*j), jobs))
+        futs = {i: ex.submit(_compile, *jobs[i]) for i in order}
+        results = [futs[i].result() for i in range(len(jobs))]
     if verbose:
         for obj, err in results:
             if err.strip():
