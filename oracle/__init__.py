@@ -91,28 +91,3 @@ def conv_single(I, F, threads: int | None = None):
     if I.ndim != 2 or F.ndim != 3:
         raise ValueError("expected I[Wy,Wx] and F[M,K,K]")
     return conv_multi(I[None], F[:, None], threads=threads)
-
-
-def conv_multi_at(I, F, points):
-    """Eq. 1 evaluated at selected outputs only.
-
-    ``points`` is an integer array of ``(m, y, x)`` rows.  Each output is
-    computed by the same C routine on the K x K window (all channels) that
-    produces it, so the fp64 sum runs in the same order as a full evaluation.
-    Used to check full-size workloads on a sample.  Returns ``(O64, A64)`` as
-    1-D float64 arrays.
-    """
-    I = np.asarray(I, dtype=np.float32)
-    F = np.asarray(F, dtype=np.float32)
-    C, Wy, Wx = I.shape
-    M, _, K, _ = F.shape
-    pts = np.asarray(points, dtype=np.int64).reshape(-1, 3)
-    O = np.empty(len(pts), dtype=np.float64)
-    A = np.empty(len(pts), dtype=np.float64)
-    for n, (m, y, x) in enumerate(pts):
-        if not (0 <= m < M and 0 <= y <= Wy - K and 0 <= x <= Wx - K):
-            raise IndexError("output (%d, %d, %d) out of range" % (m, y, x))
-        o, a = conv_multi(I[:, y:y + K, x:x + K], F[m:m + 1], threads=1)
-        O[n] = o[0, 0, 0]
-        A[n] = a[0, 0, 0]
-    return O, A

@@ -334,7 +334,8 @@ __global__ __launch_bounds__(kBlock, (Occupancy<K, VEC4>::value)) void single_ti
 // (the instruction reads its A operand from them directly).
 //
 // Sixteen blocks side by side make a 4-row x 64-column patch, and a wave
-// owns a column of P = 8 patches (32 rows x 64 columns).  It streams the
+// owns a column of P = 4 patches (16 rows x 64 columns; the four waves of a
+// workgroup make a 16 x 256 tile).  It streams the
 // input rows of that column through registers once: lane 4b + j holds
 // input row u + j (four steps t at a time, one 16-byte LDS read), which is
 // row j + r of patch p for r = u - 4p, so one read feeds every patch with

@@ -66,7 +66,7 @@ SINGLE_SHAPES = [
     (258, 70, 2, 4), (520, 65, 7, 2), (61, 200, 9, 1), (130, 45, 11, 3), (100, 80, 13, 2),
     (64, 64, 16, 1), (33, 40, 1, 5), (1030, 9, 4, 1), (96, 96, 6, 37), (80, 81, 8, 1),
     (90, 91, 10, 2),
-    # matrix-core kernel: tails of its 32 x 256 tiles and 4 x 64 patches, K = 5..11
+    # matrix-core kernel: tails of its 16 x 256 tiles and 4 x 64 patches, K = 5..11
     (300, 70, 11, 2), (516, 41, 9, 1), (264, 100, 7, 3), (12, 12, 11, 1), (20, 37, 5, 4),
     (68, 9, 8, 2), (1028, 35, 10, 1), (256, 256, 6, 1),
     # large maps with K >= 8: ragged last tile column and row, unequal tile

@@ -85,17 +85,6 @@ def test_thread_count_does_not_change_result():
     assert np.array_equal(O1, O2) and np.array_equal(A1, A2)
 
 
-def test_sampled_points_match_full_evaluation():
-    I, F = random_arrays(3, 4, 15, 12, 4, 8)
-    O, A = oracle.conv_multi(I, F, threads=1)
-    pts = np.array([[0, 0, 0], [3, 8, 11], [1, 4, 7], [2, 8, 0]])
-    o, a = oracle.conv_multi_at(I, F, pts)
-    assert np.array_equal(o, O[pts[:, 0], pts[:, 1], pts[:, 2]])
-    assert np.array_equal(a, A[pts[:, 0], pts[:, 1], pts[:, 2]])
-    with pytest.raises(IndexError):
-        oracle.conv_multi_at(I, F, [[0, 9, 0]])
-
-
 def test_rejects_bad_sizes():
     I, F = random_arrays(1, 1, 4, 4, 3, 0)
     with pytest.raises(ValueError):
