@@ -36,8 +36,22 @@ SWEEP = "single_4096x4096_m1_k3-11"
 DEFAULT_STEP = "dconv_configs"
 # Named multi-launch steps: the default (the single-map sweep and the six
 # multi-channel layers), the single-map sweep alone, single-map layers with
-# many filters, the multi-channel layers alone, and the paper's layer sweep.
-SWEEPS = (DEFAULT_STEP, SWEEP, "single_multi_filter", "multi_layers", "paper_multi_sweep")
+# many filters, the multi-channel layers alone, the paper's layer sweep, two
+# large-filter multi-channel layers, and 4096-wide maps of 1 to 8 rounds of
+# tiles per workgroup.
+SWEEPS = (DEFAULT_STEP, SWEEP, "single_multi_filter", "multi_layers", "paper_multi_sweep",
+          "large_filter_layers", "single_rounds")
+
+
+def step_names(workload):
+    """The workloads of a named step, or [workload] for a single one."""
+    import dconv_workloads as dw
+    steps = {DEFAULT_STEP: list(dw.SINGLE_4096_SWEEP) + list(dw.MULTI_CONFIGS),
+             SWEEP: list(dw.SINGLE_4096_SWEEP), "single_multi_filter": list(dw.SINGLE_MULTI_FILTER),
+             "multi_layers": list(dw.MULTI_CONFIGS), "paper_multi_sweep": list(dw.PAPER_MULTI_SWEEP),
+             "large_filter_layers": list(dw.LARGE_FILTER_LAYERS),
+             "single_rounds": list(dw.SINGLE_ROUNDS)}
+    return steps.get(workload, [workload])
 # Sources each kernel family is built from: recorded HBM traffic stays valid
 # while these are unchanged.
 SINGLE_SOURCES = ("single.hip", "xcd.h")
@@ -51,8 +65,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=50)
     ap.add_argument("--warmup", type=int, default=5)
     ap.add_argument("--workload", default=DEFAULT_STEP,
-                    help="%s (default), %s, %s, %s, %s, or a name from dconv_workloads.WORKLOADS"
-                         % SWEEPS)
+                    help="%s (default), %s, or a name from dconv_workloads.WORKLOADS"
+                         % (SWEEPS[0], ", ".join(SWEEPS[1:])))
     ap.add_argument("--variant", default="auto", choices=["auto", "mfma", "valu"],
                     help="kernel family: multi-channel workloads; for the single map, "
                          "mfma runs the matrix-core kernel where it exists (K = 5 ... 11)")
@@ -272,10 +286,7 @@ def collect_counters(out_dir, workload, variant):
     and pass (each under a 120 s limit), plus the plain-copy calibration of
     FETCH_SIZE / WRITE_SIZE.  Never touches the GPU itself."""
     import subprocess
-    from dconv_workloads import MULTI_CONFIGS, SINGLE_4096_SWEEP
-    steps = {DEFAULT_STEP: list(SINGLE_4096_SWEEP) + list(MULTI_CONFIGS),
-             SWEEP: list(SINGLE_4096_SWEEP), "multi_layers": list(MULTI_CONFIGS)}
-    names = steps.get(workload, [workload])
+    names = step_names(workload)
     here = os.path.abspath(__file__)
     runs = []
     for n in names:
@@ -345,10 +356,8 @@ def trace_report(root, workload=DEFAULT_STEP, out_path=None, command=None):
     import re
     from collections import defaultdict
     import paper_2212_00404_amd as dc
-    from dconv_workloads import MULTI_CONFIGS, SINGLE_4096_SWEEP, WORKLOADS
-    steps = {DEFAULT_STEP: list(SINGLE_4096_SWEEP) + list(MULTI_CONFIGS),
-             SWEEP: list(SINGLE_4096_SWEEP), "multi_layers": list(MULTI_CONFIGS)}
-    names = steps.get(workload, [workload])
+    from dconv_workloads import WORKLOADS
+    names = step_names(workload)
     key = {}
     for n in names:
         w = WORKLOADS[n]
@@ -767,14 +776,7 @@ def main():
         heldout(args.heldout, args.steps, args.warmup, report_out=args.report_out)
         return
     if args.autotune:
-        from dconv_workloads import WORKLOADS
-        from dconv_workloads import MULTI_CONFIGS, PAPER_MULTI_SWEEP
-        from dconv_workloads import SINGLE_4096_SWEEP, SINGLE_MULTI_FILTER
-        names = {"paper_multi_sweep": list(PAPER_MULTI_SWEEP), SWEEP: list(SINGLE_4096_SWEEP),
-                 "single_multi_filter": list(SINGLE_MULTI_FILTER),
-                 DEFAULT_STEP: list(SINGLE_4096_SWEEP) + list(MULTI_CONFIGS)}.get(
-            args.workload, [args.workload] if args.workload not in SWEEPS else list(MULTI_CONFIGS))
-        autotune(names, args.steps, args.warmup, args.report_out)
+        autotune(step_names(args.workload), args.steps, args.warmup, args.report_out)
         return
     if args.collect_counters:
         collect_counters(args.collect_counters, args.workload, args.variant)
@@ -791,13 +793,9 @@ def main():
 
     import torch
     import paper_2212_00404_amd as dc
-    from dconv_workloads import (MULTI_CONFIGS, PAPER_MULTI_SWEEP, SINGLE_4096_SWEEP,
-                                 SINGLE_MULTI_FILTER, WORKLOADS, make)
+    from dconv_workloads import WORKLOADS, make
 
-    sweeps = {DEFAULT_STEP: list(SINGLE_4096_SWEEP) + list(MULTI_CONFIGS),
-              SWEEP: list(SINGLE_4096_SWEEP), "single_multi_filter": list(SINGLE_MULTI_FILTER),
-              "multi_layers": list(MULTI_CONFIGS), "paper_multi_sweep": list(PAPER_MULTI_SWEEP)}
-    names = sweeps.get(args.workload, [args.workload])
+    names = step_names(args.workload)
     for n in names:
         if n not in WORKLOADS:
             sys.exit("unknown workload %s" % n)
@@ -956,7 +954,7 @@ def main():
         config = {"workload": SWEEP, "kind": "single", "Wx": 4096, "Wy": 4096, "M": 1, "C": 1,
                   "K": [3, 5, 7, 9, 11], "launches_per_step": 5, "variant": args.variant,
                   "buffers": "separate I/O per K (670 MB per step)"}
-    elif args.workload in sweeps:
+    elif args.workload in SWEEPS:
         config = {"workload": args.workload, "kind": bufs[0][0].kind,
                   "workloads": [b[0].name for b in bufs], "variant": args.variant,
                   "launches_per_step": len(bufs)}
@@ -984,7 +982,20 @@ def main():
 
 
 def _command_line():
-    return "python3 bench.py " + " ".join(sys.argv[1:])
+    """This run's command, with the report and result paths shown as <file> and
+    <dir> (any path works there)."""
+    out, skip = [], None
+    for a in sys.argv[1:]:
+        if skip:
+            out.append(skip)
+            skip = None
+            continue
+        out.append(a)
+        if a == "--report-out":
+            skip = "<file>"
+        elif a in ("--collect-counters", "--counter-report", "--trace-report"):
+            skip = "<dir>"
+    return "python3 bench.py " + " ".join(out)
 
 
 def write_step_report(out, path):

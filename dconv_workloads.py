@@ -103,6 +103,11 @@ WORKLOADS = {w.name: w for w in [
         (64, 512, 3), (64, 224, 3), (128, 112, 3), (256, 56, 3), (512, 28, 3), (512, 14, 3),
         (512, 7, 3), (64, 56, 1), (256, 28, 1), (512, 14, 1), (64, 56, 5), (128, 28, 5),
         (256, 14, 5))],
+    # 4096-wide single maps of 1, 2, 4 and 8 rounds of tiles per persistent
+    # workgroup (K = 11: 1032, 2056, 4096, 8192 rows; K = 7: 2056, 4096,
+    # 8192): the time per round and the fixed cost of a launch
+    *[Workload("single_4096x%d_m1_k%d" % (h, k), "single", 1, 1, 4096, h, k)
+      for k, hs in ((11, (1032, 2056, 8192)), (7, (2056, 8192))) for h in hs],
 ]}
 
 # The large single-map workload is one pass over all five filter sizes.
@@ -113,6 +118,12 @@ MULTI_CONFIGS = ("multi_c512_9x9_m512_k3", "multi_c256_30x30_m256_k3", "multi_c5
                  "multi_c256_28x28_m256_k1")
 # The paper's multi-channel layer sweep.
 PAPER_MULTI_SWEEP = tuple(n for n in WORKLOADS if n.startswith("layer_"))
+# Large filters on small multi-channel maps.
+LARGE_FILTER_LAYERS = ("multi_c64_40x40_m64_k9", "multi_c32_42x42_m64_k11")
+# The 4096-wide single map at 1, 2, 4 and 8 rounds of tiles per workgroup.
+SINGLE_ROUNDS = ("single_4096x1032_m1_k11", "single_4096x2056_m1_k11", "single_4096x4096_m1_k11",
+                 "single_4096x8192_m1_k11", "single_4096x2056_m1_k7", "single_4096x4096_m1_k7",
+                 "single_4096x8192_m1_k7")
 # Single map, many filters.
 SINGLE_MULTI_FILTER = ("single_28x28_m512_k3", "single_56x56_m256_k5", "single_112x112_m128_k3",
                        "single_224x224_m64_k5", "single_512x512_m128_k1",

@@ -718,13 +718,14 @@ int plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, int vari
   p->K = K;
   // 16-byte aligned rows: whole float4 staging loads.
   const bool vec4 = aligned && (Wx % 4 == 0);
-  // The matrix-core kernel needs float4 staging.  It runs only when forced:
-  // measured on a 4096 x 4096 map it ties the vector kernel at K = 7 and
-  // trails it at K = 9 (52 vs 44 us) and K = 11 (67 vs 58 us), so the
-  // automatic choice is the vector kernel.
+  // The matrix-core kernel needs float4 staging.  On a 4096 x 4096 map it
+  // is 5-9% faster than the vector kernel at K = 7 and slower at K = 5
+  // (31 vs 28 us), K = 9 (54 vs 47 us) and K = 11 (72 vs 63 us), so the
+  // automatic choice takes it at K = 7 only.
   const bool can_mfma = vec4 && K >= kMfmaMinK && K <= kMaxTiledK;
   if (variant == DCONV_VARIANT_MFMA && !can_mfma) return DCONV_EUNSUPPORTED;
-  const bool mfma = variant == DCONV_VARIANT_MFMA;
+  const bool mfma =
+      variant == DCONV_VARIANT_MFMA || (variant == DCONV_VARIANT_AUTO && can_mfma && K == 7);
   switch (K) {
 #define DCONV_PLAN_K(k)                                              \
   case k:                                                            \

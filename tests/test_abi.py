@@ -178,13 +178,17 @@ def test_single_plan_shapes(shape):
             dc.plan_single(*shape, variant="mfma")
 
 
-def test_single_auto_uses_the_vector_kernel():
-    """The matrix-core single-map kernel runs only when forced (it measured
-    slower than the vector kernel for every K on a 4096 x 4096 map)."""
+def test_single_auto_takes_the_matrix_cores_at_k7_only():
+    """The automatic single-map plan runs the matrix-core kernel at K = 7,
+    where it measured faster than the vector kernel on a 4096 x 4096 map, and
+    the vector kernel for every other K (and for rows that are not whole
+    float4, which the matrix-core kernel cannot stage)."""
     for K in range(1, 12):
-        assert dc.plan_single(4096, 4096, K, 1)["kernel"] == 0, K
+        assert dc.plan_single(4096, 4096, K, 1)["kernel"] == (3 if K == 7 else 0), K
         if K >= 5:
             assert dc.plan_single(4096, 4096, K, 1, variant="mfma")["kernel"] == 3
+    # rows of 4097 floats: the vector kernel's unaligned-row form
+    assert dc.plan_single(4097, 4096, 7, 1)["kernel"] == 2
 
 
 @pytest.mark.parametrize("shape", [
