@@ -104,10 +104,10 @@ WORKLOADS = {w.name: w for w in [
         (512, 7, 3), (64, 56, 1), (256, 28, 1), (512, 14, 1), (64, 56, 5), (128, 28, 5),
         (256, 14, 5))],
     # 4096-wide single maps of 1, 2, 4 and 8 rounds of tiles per persistent
-    # workgroup (K = 11: 1032, 2056, 4096, 8192 rows; K = 7: 2056, 4096,
-    # 8192): the time per round and the fixed cost of a launch
+    # workgroup (K = 9 and 11: 1032, 2056, 4096, 8192 rows): the time per
+    # round and the fixed cost of a launch
     *[Workload("single_4096x%d_m1_k%d" % (h, k), "single", 1, 1, 4096, h, k)
-      for k, hs in ((11, (1032, 2056, 8192)), (7, (2056, 8192))) for h in hs],
+      for k in (9, 11) for h in (1032, 2056, 8192)],
 ]}
 
 # The large single-map workload is one pass over all five filter sizes.
@@ -121,9 +121,8 @@ PAPER_MULTI_SWEEP = tuple(n for n in WORKLOADS if n.startswith("layer_"))
 # Large filters on small multi-channel maps.
 LARGE_FILTER_LAYERS = ("multi_c64_40x40_m64_k9", "multi_c32_42x42_m64_k11")
 # The 4096-wide single map at 1, 2, 4 and 8 rounds of tiles per workgroup.
-SINGLE_ROUNDS = ("single_4096x1032_m1_k11", "single_4096x2056_m1_k11", "single_4096x4096_m1_k11",
-                 "single_4096x8192_m1_k11", "single_4096x2056_m1_k7", "single_4096x4096_m1_k7",
-                 "single_4096x8192_m1_k7")
+SINGLE_ROUNDS = tuple("single_4096x%d_m1_k%d" % (h, k) for k in (9, 11)
+                      for h in (1032, 2056, 4096, 8192))
 # Single map, many filters.
 SINGLE_MULTI_FILTER = ("single_28x28_m512_k3", "single_56x56_m256_k5", "single_112x112_m128_k3",
                        "single_224x224_m64_k5", "single_512x512_m128_k1",
