@@ -719,9 +719,10 @@ int plan_single(int Wx, int Wy, int K, int M, int num_cu, bool aligned, int vari
   // 16-byte aligned rows: whole float4 staging loads.
   const bool vec4 = aligned && (Wx % 4 == 0);
   // The matrix-core kernel needs float4 staging.  On a 4096 x 4096 map it
-  // is 5-9% faster than the vector kernel at K = 7 and slower at K = 5
-  // (31 vs 28 us), K = 9 (54 vs 47 us) and K = 11 (72 vs 63 us), so the
-  // automatic choice takes it at K = 7 only.
+  // is level with the vector kernel at K = 7 (ahead in a sequence of
+  // launches of all filter sizes, behind in repeats of K = 7 alone) and
+  // slower at K = 5 (31 vs 28 us), K = 9 (54 vs 47 us) and K = 11 (72 vs
+  // 63 us), so the automatic choice takes it at K = 7 only.
   const bool can_mfma = vec4 && K >= kMfmaMinK && K <= kMaxTiledK;
   if (variant == DCONV_VARIANT_MFMA && !can_mfma) return DCONV_EUNSUPPORTED;
   const bool mfma =
