@@ -89,6 +89,11 @@ def parse():
     ap.add_argument("--copy-probe", type=int, default=0, metavar="MIB",
                     help="instead of convolving, copy a MIB-sized device buffer --steps "
                          "times (reference kernel for scaling HBM byte counters)")
+    ap.add_argument("--stage-trace", action="store_true",
+                    help="run each multi-channel workload of the step on the stage-trace build "
+                         "(libdconv_trace.so) and report where a stage's clocks go (copy wait, "
+                         "barrier, issuing the next stage's copies, MFMAs) for the first and "
+                         "the last wave of every workgroup; --report-out names the file")
     ap.add_argument("--peaks", action="store_true",
                     help="instead of convolving, run the peak microbenchmarks (HBM read, write "
                          "and copy streams, fp32 FMA, fp32 MFMA 32x32x2 and 16x16x4, global->LDS "
@@ -768,6 +773,10 @@ def main():
     if args.latency_probe:
         latency_probe()
         return
+    if args.stage_trace:
+        stage_trace(args.workload if args.workload != DEFAULT_STEP else "multi_layers",
+                    args.warmup, args.report_out)
+        return
     if args.peaks:
         from paper_2212_00404_amd import peaks
         print(json.dumps({"peaks": peaks.run()}), flush=True)
@@ -979,6 +988,93 @@ def main():
     print(json.dumps(out), flush=True)
     if args.report_out:
         write_step_report(out, args.report_out)
+
+
+def stage_trace(workload, warmup, report_out=None):
+    """Stage-loop timeline of the multi-channel matrix-core kernel from the
+    stage-trace build (libdconv_trace.so, -DDCONV_STAGE_TRACE): per workload
+    of the step, the planner's plan launched warmup + 1 times with a trace
+    buffer registered; the last launch's records (two per workgroup: wave 0
+    and the last wave) are summarised as medians over workgroups, in shader
+    clocks and microseconds.  The trace's own global stores add a little to
+    every phase."""
+    import ctypes
+    import torch
+    import paper_2212_00404_amd as dc
+    from paper_2212_00404_amd import build as pb
+    from dconv_workloads import WORKLOADS, make
+    stages_max, words = 64, 6 + 5 * 64
+    lib = dc.load(pb.TRACE_LIB)
+    lib.dconv_debug_stage_trace.argtypes = [ctypes.c_void_p]
+    lib.dconv_debug_stage_trace.restype = None
+    dev = torch.device("cuda:0")
+    stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+    results = []
+    for n in step_names(workload):
+        w = WORKLOADS[n]
+        if w.kind != "multi":
+            continue
+        p = dc.plan_multi(w.C, w.M, w.Wx, w.Wy, w.K)
+        if p["variant"] != 2:
+            continue
+        I, F = make(w)
+        It, Ft = torch.from_numpy(I).to(dev), torch.from_numpy(F).to(dev)
+        Ot = torch.empty((w.M, w.Hout, w.Wout), device=dev)
+        buf = torch.zeros(p["grid_x"] * 2 * words, dtype=torch.int64, device=dev)
+        lib.dconv_debug_stage_trace(ctypes.c_void_p(buf.data_ptr()))
+        for _ in range(warmup + 1):
+            rc = lib.dconv_multi(ctypes.c_void_p(It.data_ptr()), ctypes.c_void_p(Ft.data_ptr()),
+                                 ctypes.c_void_p(Ot.data_ptr()), w.C, w.M, w.Wx, w.Wy, w.K,
+                                 stream)
+            if rc != 0:
+                sys.exit("dconv_multi (trace build) failed: %d" % rc)
+        torch.cuda.synchronize()
+        lib.dconv_debug_stage_trace(None)
+        t = buf.cpu().numpy().reshape(p["grid_x"], 2, words).astype(np.float64)
+        first = t[:, 0, :]
+        ok = (first[:, 5] > first[:, 0]) & (first[:, 4] > first[:, 1])
+        ghz = float(np.median((first[ok, 4] - first[ok, 1]) / (first[ok, 5] - first[ok, 0]))) / 10.0
+        nst = min(-(-w.C // p["chunk_c"]), stages_max)
+        med = lambda x: float(np.median(x))
+
+        def phases(rec):
+            out = []
+            for k in range(4):   # wait, barrier, issue, compute
+                vals = [rec[:, 6 + 5 * s + k + 1] - rec[:, 6 + 5 * s + k] for s in range(nst)]
+                out.append(med(np.concatenate(vals)))
+            return out
+        res = {"workload": n, "plan": "k%d/m%d/%dx%d/c%d/w%d/%dwaves" % (
+                   p["kernel"], p["tile_m"], p["tile_h"], p["tile_w"], p["chunk_c"], p["waves_c"],
+                   p["block"] // 64),
+               "workgroups": p["grid_x"], "stages": -(-w.C // p["chunk_c"]),
+               "clock_ghz": round(ghz, 2),
+               "setup": med(first[:, 2] - first[:, 1]), "first_copies": med(first[:, 3] - first[:, 2]),
+               "wave0": phases(first), "last_wave": phases(t[:, 1, :]),
+               "span_us": med(first[:, 5] - first[:, 0]) / 100.0}
+        results.append(res)
+        print(json.dumps(res), flush=True)
+    if report_out:
+        lines = ["# Stage timeline of the multi-channel matrix-core kernel", "", "Command:", "",
+                 "```", _command_line(), "```", "",
+                 "The stage-trace build (`libdconv_trace.so`, `-DDCONV_STAGE_TRACE`) records the "
+                 "shader clock around each phase of the stage loop in wave 0 and in the last "
+                 "wave of every workgroup; medians over workgroups and stages, in clocks (the "
+                 "trace's own stores add a little to each phase).  Per stage: wait = this wave's "
+                 "copies of the stage landing, barrier = every wave arriving, issue = issuing "
+                 "the next stage's copies, MFMAs = the stage's matrix instructions.  Setup = "
+                 "kernel start to the first copies; first copies = issuing stage 0; span = "
+                 "kernel start to end of wave 0 (wall clock).", "",
+                 "| workload | plan | workgroups | stages | clock GHz | setup | first copies | "
+                 "wave 0: wait / barrier / issue / MFMAs | last wave: wait / barrier / issue / "
+                 "MFMAs | span us |",
+                 "|---|---|---|---|---|---|---|---|---|---|"]
+        for r in results:
+            lines.append("| %s | `%s` | %d | %d | %.2f | %d | %d | %s | %s | %.2f |" % (
+                r["workload"], r["plan"], r["workgroups"], r["stages"], r["clock_ghz"],
+                r["setup"], r["first_copies"], " / ".join("%d" % v for v in r["wave0"]),
+                " / ".join("%d" % v for v in r["last_wave"]), r["span_us"]))
+        with open(report_out, "w") as fh:
+            fh.write("\n".join(lines) + "\n")
 
 
 def _command_line():

@@ -25,6 +25,10 @@ LIB = os.path.join(PKG, "libdconv.so")
 # (-DDCONV_POISON_LDS): a GPU test runs it to catch reads of LDS that a
 # kernel did not write first.
 POISON_LIB = os.path.join(PKG, "libdconv_poison.so")
+# Debug build whose multi-channel matrix-core kernel records clock counters
+# around the phases of its stage loop (-DDCONV_STAGE_TRACE; bench.py
+# --stage-trace reads them).
+TRACE_LIB = os.path.join(PKG, "libdconv_trace.so")
 PEAKS_SRC = os.path.join(PKG, "peaks", "peaks.hip")
 PEAKS_LIB = os.path.join(PKG, "libdconv_peaks.so")
 ARCH = "gfx950"
@@ -108,14 +112,18 @@ def _link(objs, lib):
 
 
 def build(verbose: bool = False) -> str:
-    """Compile every source and link the library, its LDS-poisoning debug
-    twin (libdconv_poison.so) and the peak microbenchmarks
-    (libdconv_peaks.so, from peaks/); returns the library's path."""
+    """Compile every source and link the library, its LDS-poisoning and
+    stage-trace debug twins (libdconv_poison.so, libdconv_trace.so) and the
+    peak microbenchmarks (libdconv_peaks.so, from peaks/); returns the
+    library's path."""
     poison_dir = os.path.join(BUILD, "poison")
+    trace_dir = os.path.join(BUILD, "trace")
     os.makedirs(poison_dir, exist_ok=True)
+    os.makedirs(trace_dir, exist_ok=True)
     srcs = sorted(glob.glob(os.path.join(CSRC, "*.hip")))
     jobs = ([(s, BUILD, ()) for s in srcs] + [(PEAKS_SRC, BUILD, ())] +
-            [(s, poison_dir, ("-DDCONV_POISON_LDS",)) for s in srcs])
+            [(s, poison_dir, ("-DDCONV_POISON_LDS",)) for s in srcs] +
+            [(s, trace_dir, ("-DDCONV_STAGE_TRACE",)) for s in srcs])
     workers = min(len(jobs), max(1, min(8, os.cpu_count() or 1)))
     # the matrix-core kernel units take longest: start them first
     order = sorted(range(len(jobs)), key=lambda i: "multi_mfma" not in jobs[i][0])
@@ -130,7 +138,8 @@ def build(verbose: bool = False) -> str:
     n = len(srcs)
     _link(objs[:n], LIB)
     _link(objs[n:n + 1], PEAKS_LIB)
-    _link(objs[n + 1:], POISON_LIB)
+    _link(objs[n + 1:2 * n + 1], POISON_LIB)
+    _link(objs[2 * n + 1:], TRACE_LIB)
     return LIB
 
 

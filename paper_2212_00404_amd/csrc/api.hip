@@ -165,6 +165,13 @@ DCONV_EXPORT int dconv_multi_variant(const float *I, const float *F, float *O, i
   return run_multi(p, I, F, O, C, M, Wx, Wy, (hipStream_t)stream);
 }
 
+#ifdef DCONV_STAGE_TRACE
+// Trace builds only (not declared in dconv.h): register the buffer the
+// multi-channel matrix-core kernel writes its stage-trace records to
+// (2 * grid_x * kStageTraceWords long longs, device memory), or NULL.
+DCONV_EXPORT void dconv_debug_stage_trace(long long *buf) { dconv::g_stage_trace = buf; }
+#endif
+
 DCONV_EXPORT int dconv_multi_with_plan(const float *I, const float *F, float *O, int C, int M,
                                        int Wx, int Wy, int K, const dconv_plan *plan,
                                        void *stream) {

@@ -33,6 +33,23 @@ __device__ __forceinline__ void poison_lds(T *p, int n) {
   } while (0)
 #endif
 
+// Stage-trace debug builds (-DDCONV_STAGE_TRACE, libdconv_trace.so): the
+// multi-channel matrix-core kernel records clock counters around the phases
+// of its stage loop into a buffer the caller registers with
+// dconv_debug_stage_trace() (kStageTraceWords long longs per record, two
+// records per workgroup: wave 0 and the last wave).  Record layout: [0] start
+// (wall clock, 100 MHz), [1] start (shader clock), [2] before the first
+// stage's copies, [3] after them, [4] after the stage loop (and channel-group
+// sum), [5] end (wall clock), then for stage s < kStageTraceStages the shader
+// clock at [6 + 5s + i]: i = 0 stage start, 1 after the copy wait, 2 after
+// the barrier, 3 after issuing the next stage's copies, 4 after the MFMAs.
+// Ordinary builds: none of this.
+constexpr int kStageTraceStages = 64;
+constexpr int kStageTraceWords = 6 + 5 * kStageTraceStages;
+#ifdef DCONV_STAGE_TRACE
+extern long long *g_stage_trace;
+#endif
+
 // ---------------------------------------------------------------------------
 // Single-map kernels (Eq. 2)
 // ---------------------------------------------------------------------------

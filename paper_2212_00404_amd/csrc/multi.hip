@@ -5,6 +5,9 @@
 #include "multi_kernels.h"
 
 namespace dconv {
+#ifdef DCONV_STAGE_TRACE
+long long *g_stage_trace = nullptr;
+#endif
 namespace {
 
 // ---------------------------------------------------------------------------
@@ -294,6 +297,9 @@ hipError_t launch_multi(const MultiPlan &p, const float *I, const float *F, floa
   a.IH = p.tpy + p.K - 1;
   a.IW = p.tpx + p.K - 1;
   a.ICS = a.IH * a.IW;
+#ifdef DCONV_STAGE_TRACE
+  a.trace = g_stage_trace;
+#endif
   if (p.kernel == kGenericKernel) {
     hipLaunchKernelGGL(multi_generic, dim3(p.grid_x), dim3(256), 0, st, I, F, O, C, M, Wx, Wy, p.K);
     return hipGetLastError();

@@ -49,6 +49,7 @@ struct TileArgs {
   int ntiles;         // output tiles per map
   int mtiles;         // filter tiles
   int IH, IW, ICS;    // staged input tile rows, columns, channel stride
+  long long *trace;   // stage-trace records (trace builds only; null otherwise)
 };
 
 // The launchers of the matrix-core kernels for one filter size each,
@@ -301,6 +302,10 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
                                                                const float *__restrict__ F,
                                                                float *__restrict__ O, TileArgs a) {
   using Cfg = MfmaCfg<K, MF, MB, NB, WM, WN, WC, DEEP>;
+#ifdef DCONV_STAGE_TRACE
+  const long long tr_clock0 = clock64();
+  const long long tr_wall0 = wall_clock64();
+#endif
   using Op = Mfma<MF>;
   using acc_t = typename Op::acc;
   constexpr int KK = Cfg::KK, MT = Cfg::MT, CC = Cfg::CC, CCW = Cfg::CCW, FROW = Cfg::FROW;
@@ -328,6 +333,25 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   const int wm = wmn % WM;
   const int wn = wmn / WM;
   const int col = lane % MF;   // filter row of A / pixel of B this lane supplies
+  // Stage trace (trace builds): lane 0 of wave 0 and of the last wave writes
+  // the shader clock into word idx of its record.
+  [[maybe_unused]] const int tr_sel = wave == 0 ? 0 : (wave == NW - 1 ? 1 : -1);
+  auto mark = [&](int idx) __attribute__((always_inline)) {
+#ifdef DCONV_STAGE_TRACE
+    const long long t = clock64();
+    if (a.trace && tr_sel >= 0 && lane == 0)
+      a.trace[((size_t)blockIdx.x * 2 + tr_sel) * kStageTraceWords + idx] = t;
+#else
+    (void)idx;
+#endif
+  };
+#ifdef DCONV_STAGE_TRACE
+  if (a.trace && tr_sel >= 0 && lane == 0) {
+    long long *rec = a.trace + ((size_t)blockIdx.x * 2 + tr_sel) * kStageTraceWords;
+    rec[0] = tr_wall0;
+    rec[1] = tr_clock0;
+  }
+#endif
   const int grp = lane / MF;   // which of the KG channels of a k-step
 
   int a_base[MB];
@@ -603,12 +627,21 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     constexpr int j = decltype(J)::value;
     float *cur = j == 0 ? buf0 : buf1;
     float *nxt = j == 0 ? buf1 : buf0;
+    const int st = cs / CC;
+    const int tw = st < kStageTraceStages ? 6 + 5 * st : -1;
+    if (tw >= 0) mark(tw);
     wait_lds_dma();
+    if (tw >= 0) mark(tw + 1);
     lds_barrier();
+    if (tw >= 0) mark(tw + 2);
     if (cs + CC < c_end) issue(cs + CC, nxt);
+    if (tw >= 0) mark(tw + 3);
     compute(cur);
+    if (tw >= 0) mark(tw + 4);
   };
+  mark(2);
   issue(0, buf0);
+  mark(3);
   for (int c0 = 0; c0 < c_end; c0 += 2 * CC) {
     stage(std::integral_constant<int, 0>{}, c0);
     if (c0 + CC >= c_end) break;
@@ -643,6 +676,11 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
             acc[mb][nb][v] += red[((((g - 1) * WM * WN + wmn) * MB + mb) * NB + nb) * ACC + v * 64 + lane];
   }
 
+  mark(4);
+#ifdef DCONV_STAGE_TRACE
+  if (a.trace && tr_sel >= 0 && lane == 0)
+    a.trace[((size_t)blockIdx.x * 2 + tr_sel) * kStageTraceWords + 5] = wall_clock64();
+#endif
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) {
     const int p = wn * MF * NB + nb * MF + col;

@@ -246,3 +246,17 @@ def test_source_digest_ignores_comments_only():
     assert _code_only(a) == _code_only(b)
     assert _code_only('s = "//kept";') == 's = "//kept";'
     assert _code_only("x = 1;") != _code_only("x = 2;")
+
+
+def test_debug_builds_export_the_api():
+    """The LDS-poisoning and stage-trace twins export the same entry points,
+    the trace build one more (its buffer registration), which the ordinary
+    library does not have."""
+    import subprocess
+    for lib, extra in (("libdconv_poison.so", set()),
+                       ("libdconv_trace.so", {"dconv_debug_stage_trace"})):
+        path = os.path.join(os.path.dirname(dc.dconv.LIB_PATH), lib)
+        out = subprocess.run(["nm", "-D", "--defined-only", path],
+                             capture_output=True, text=True, check=True).stdout
+        syms = {l.split()[-1] for l in out.splitlines() if " T " in l}
+        assert syms == set(dc.EXPORTED) | extra, (lib, syms ^ (set(dc.EXPORTED) | extra))
