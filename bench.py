@@ -110,6 +110,8 @@ def parse():
                     help="time every matrix-core candidate plan of N seeded random layer shapes "
                          "(not the ones the planner's model was fitted on) and the planner's "
                          "choice; one JSON line per shape")
+    ap.add_argument("--heldout-seed", type=int, default=20221230,
+                    help="seed of the --heldout shape generator")
     ap.add_argument("--autotune", action="store_true",
                     help="for the multi-channel workload(s), time every candidate plan, the "
                          "planner's choice and the paper-rule choice; one JSON line per workload")
@@ -239,7 +241,8 @@ def heldout(n, steps, warmup, seed=20221230, report_out=None):
         res = {"shape": {"C": C, "M": M, "Wx": Wx, "Wy": Wy, "K": K},
                "candidates": len(times), "best": best, "best_us": round(times[best], 2),
                "planner": planner, "planner_us": round(times[planner], 2),
-               "planner_over_best": round(times[planner] / times[best], 3)}
+               "planner_over_best": round(times[planner] / times[best], 3),
+               "us": {t: round(v, 2) for t, v in times.items()}}
         results.append(res)
         print(json.dumps(res), flush=True)
     if report_out:
@@ -782,7 +785,8 @@ def main():
         print(json.dumps({"peaks": peaks.run()}), flush=True)
         return
     if args.heldout:
-        heldout(args.heldout, args.steps, args.warmup, report_out=args.report_out)
+        heldout(args.heldout, args.steps, args.warmup, seed=args.heldout_seed,
+                report_out=args.report_out)
         return
     if args.autotune:
         autotune(step_names(args.workload), args.steps, args.warmup, args.report_out)
