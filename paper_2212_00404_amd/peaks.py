@@ -34,8 +34,11 @@ def load():
         lib.peaks_mfma.argtypes = [vp, i, i, i, vp]
         lib.peaks_lds_dma.argtypes = [vp, ll, i, i, i, vp, i, vp]
         lib.peaks_lds_dma_layout.argtypes = [vp, i, i, vp, vp]
+        lib.peaks_vgpr_load.argtypes = [vp, ll, i, vp, i, vp]
+        lib.peaks_mfma_chains.argtypes = [vp, i, i, i, vp]
         for f in ("peaks_hbm_read", "peaks_hbm_write", "peaks_hbm_copy", "peaks_fma",
-                  "peaks_mfma", "peaks_lds_dma", "peaks_lds_dma_layout"):
+                  "peaks_mfma", "peaks_lds_dma", "peaks_lds_dma_layout", "peaks_vgpr_load",
+                  "peaks_mfma_chains"):
             getattr(lib, f).restype = i
         _lib = lib
     return _lib
@@ -89,11 +92,20 @@ def run(reps: int = 10, hbm_mib: int = 2048) -> dict:
     out = torch.empty(grid * 256, dtype=torch.float32, device=dev)
     ms = _time(lambda s: _rc(lib.peaks_fma(out.data_ptr(), iters, grid, sp(s))), reps)
     res["fma_fp32_tflops"] = round(grid * 256 * iters * 8 * 2 / ms / 1e9, 2)
-    # fp32 MFMA: grid x 4 waves x iters x 4 instructions x (4096 or 2048) flops
-    for shape, fl in ((32, 4096), (16, 2048)):
-        it = 4000 if shape == 32 else 8000
+    # fp32 MFMA: grid x 4 waves x iters x 4 instructions x (4096, 2048 or 512)
+    # flops
+    for shape, fl in ((32, 4096), (16, 2048), (4, 512)):
+        it = 4000 * 4096 // fl
         ms = _time(lambda s: _rc(lib.peaks_mfma(out.data_ptr(), it, grid, shape, sp(s))), reps)
         res["mfma_f32_%dx%d_tflops" % (shape, shape)] = round(grid * 4 * it * 4 * fl / ms / 1e9, 2)
+    # dependent v_mfma_f32_4x4x1f32: clocks (at 2.4 GHz) per instruction with
+    # one wave per SIMD and 1, 2, 4 or 8 independent accumulation chains
+    chains = {}
+    for na in (1, 2, 4, 8):
+        it = 32000 // na
+        ms = _time(lambda s: _rc(lib.peaks_mfma_chains(out.data_ptr(), na, it, cu, sp(s))), reps)
+        chains[str(na)] = round(ms * 1e-3 * 2.4e9 / (it * na), 1)
+    res["mfma_f32_4x4_clk_per_instr_by_chains"] = chains
     # global -> LDS copies from a 2 MiB region (L2-resident): bytes per
     # second in total and per compute unit per clock at 2.4 GHz
     # (16-byte copies also from sources one float off their alignment)
@@ -109,6 +121,26 @@ def run(reps: int = 10, hbm_mib: int = 2048) -> dict:
         key = "lds_dma_b%d%s" % (width * 8, "_unaligned" if shift else "")
         res[key + "_gbs"] = round(total / ms / 1e6, 1)
         res[key + "_bytes_per_cu_clk"] = round(total / ms / 1e-3 / cu / 2.4e9, 1)
+    # the copy rate per compute unit against the number of waves issuing
+    # copies (4 per workgroup; at most 8 fit for 16-byte copies, whose
+    # workgroups hold 64 KB of LDS)
+    by_waves = {"b32": {}, "b128": {}}
+    for width, waves in ((4, 4), (4, 8), (4, 16), (4, 32), (16, 4), (16, 8)):
+        gw = cu * waves // 4
+        ow = torch.empty(gw * 256, dtype=torch.float32, device=dev)
+        ms = _time(lambda s: _rc(lib.peaks_lds_dma(src.data_ptr(), region, 0, width, 200,
+                                                   ow.data_ptr(), gw, sp(s))), reps)
+        total = gw * 4 * 200 * 16 * 64 * width
+        by_waves["b%d" % (width * 8)][str(waves)] = round(total / ms / 1e-3 / cu / 2.4e9, 1)
+        del ow
+    res["lds_dma_bytes_per_cu_clk_by_waves_per_cu"] = by_waves
+    # the same walk into registers (float4 loads)
+    bursts = 400
+    ms = _time(lambda s: _rc(lib.peaks_vgpr_load(src.data_ptr(), region, bursts, o.data_ptr(),
+                                                 g, sp(s))), reps)
+    total = g * 4 * bursts * 16 * 64 * 16
+    res["l2_vgpr_b128_gbs"] = round(total / ms / 1e6, 1)
+    res["l2_vgpr_b128_bytes_per_cu_clk"] = round(total / ms / 1e-3 / cu / 2.4e9, 1)
     return res
 
 

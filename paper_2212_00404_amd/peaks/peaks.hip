@@ -74,7 +74,8 @@ __global__ __launch_bounds__(256) void fma_stream(float *__restrict__ out, int i
 typedef float f16v __attribute__((ext_vector_type(16)));
 
 // Four independent accumulators per wave of v_mfma_f32_32x32x2_f32
-// (4096 flops each) or v_mfma_f32_16x16x4_f32 (2048 flops each).
+// (4096 flops each), v_mfma_f32_16x16x4_f32 (2048 flops each) or
+// v_mfma_f32_4x4x1f32 (16 blocks of 4 x 4 x 1, 512 flops each).
 template <int MF>
 __global__ __launch_bounds__(256) void mfma_stream(float *__restrict__ out, int iters) {
   const float av = 1.0f + threadIdx.x * 1e-7f, bv = 1.0f - threadIdx.x * 1e-7f;
@@ -100,13 +101,37 @@ __global__ __launch_bounds__(256) void mfma_stream(float *__restrict__ out, int 
     for (int j = 0; j < 4; ++j) c[j] = f4{0.f, 0.f, 0.f, 0.f};
     for (int it = 0; it < iters; ++it) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) c[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, c[j], 0, 0, 0);
+      for (int j = 0; j < 4; ++j) {
+        if constexpr (MF == 16)
+          c[j] = __builtin_amdgcn_mfma_f32_16x16x4f32(av, bv, c[j], 0, 0, 0);
+        else
+          c[j] = __builtin_amdgcn_mfma_f32_4x4x1f32(av, bv, c[j], 0, 0, 0);
+      }
     }
     float s = 0.f;
 #pragma unroll
     for (int j = 0; j < 4; ++j) s += c[j].x + c[j].y + c[j].z + c[j].w;
     out[(int64_t)blockIdx.x * 256 + threadIdx.x] = s;
   }
+}
+
+// NA independent accumulation chains of v_mfma_f32_4x4x1f32 per wave: with
+// one wave per SIMD (grid = compute units, 256 threads) the time per
+// instruction shows how far apart dependent instructions must be.
+template <int NA>
+__global__ __launch_bounds__(256) void mfma_chains(float *__restrict__ out, int iters) {
+  const float av = 1.0f + threadIdx.x * 1e-7f, bv = 1.0f - threadIdx.x * 1e-7f;
+  f4 c[NA];
+#pragma unroll
+  for (int j = 0; j < NA; ++j) c[j] = f4{0.f, 0.f, 0.f, 0.f};
+  for (int it = 0; it < iters; ++it) {
+#pragma unroll
+    for (int j = 0; j < NA; ++j) c[j] = __builtin_amdgcn_mfma_f32_4x4x1f32(av, bv, c[j], 0, 0, 0);
+  }
+  float s = 0.f;
+#pragma unroll
+  for (int j = 0; j < NA; ++j) s += c[j].x + c[j].y + c[j].z + c[j].w;
+  out[(int64_t)blockIdx.x * 256 + threadIdx.x] = s;
 }
 
 typedef __attribute__((address_space(3))) void *lds_void_ptr;
@@ -145,6 +170,30 @@ __global__ __launch_bounds__(256) void lds_dma_stream(const float *__restrict__ 
   out[(int64_t)blockIdx.x * 256 + threadIdx.x] = buf[threadIdx.x];
 }
 
+// The same source walk as lds_dma_stream<16>, loaded into registers instead
+// (16 float4 loads in flight per lane, then a wait and a sum): the rate the
+// L2 -> vector L1 path delivers to ordinary loads, for comparison with the
+// direct copies above.
+__global__ __launch_bounds__(256) void vgpr_load_stream(const float *__restrict__ src,
+                                                        int64_t mask, int bursts,
+                                                        float *__restrict__ out) {
+  constexpr int SLOT = 256;
+  const int lane = threadIdx.x & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+  int64_t base = ((int64_t)blockIdx.x * 4 + wave) * 16 * SLOT;
+  f4 acc = f4{0.f, 0.f, 0.f, 0.f};
+  for (int b = 0; b < bursts; ++b) {
+    f4 x[16];
+#pragma unroll
+    for (int s = 0; s < 16; ++s)
+      x[s] = *reinterpret_cast<const f4 *>(src + ((base + (int64_t)s * SLOT + lane * 4) & mask));
+#pragma unroll
+    for (int s = 0; s < 16; ++s) acc += x[s];
+    base += 16 * SLOT * 7;
+  }
+  out[(int64_t)blockIdx.x * 256 + threadIdx.x] = acc.x + acc.y + acc.z + acc.w;
+}
+
 // Where a 16-byte-per-lane direct copy lands when its LDS destination is
 // `shift` floats (0 to 3) past a 16-byte boundary: one wave copies 256
 // floats of src into a zeroed LDS array at float offset shift, then writes
@@ -173,6 +222,17 @@ PEAKS_EXPORT int peaks_lds_dma_layout(const float *src, int shift, int active, f
   (void)hipGetLastError();
   hipLaunchKernelGGL(lds_dma_layout, dim3(1), dim3(64), 0, (hipStream_t)stream, src, shift, active,
                      out);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+PEAKS_EXPORT int peaks_vgpr_load(const float *src, long long region_floats, int bursts,
+                                  float *out, int grid, void *stream) {
+  if (!src || !out || bursts < 1 || grid < 1 || region_floats < 4096 ||
+      (region_floats & (region_floats - 1)) != 0)
+    return -1;
+  (void)hipGetLastError();
+  hipLaunchKernelGGL(vgpr_load_stream, dim3(grid), dim3(256), 0, (hipStream_t)stream, src,
+                     (int64_t)(region_floats - 1), bursts, out);
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
@@ -213,12 +273,27 @@ PEAKS_EXPORT int peaks_fma(float *out, int iters, int grid, void *stream) {
 }
 
 PEAKS_EXPORT int peaks_mfma(float *out, int iters, int grid, int shape, void *stream) {
-  if (!out || iters < 1 || grid < 1 || (shape != 32 && shape != 16)) return -1;
+  if (!out || iters < 1 || grid < 1 || (shape != 32 && shape != 16 && shape != 4)) return -1;
   (void)hipGetLastError();
   if (shape == 32)
     hipLaunchKernelGGL(mfma_stream<32>, dim3(grid), dim3(256), 0, (hipStream_t)stream, out, iters);
-  else
+  else if (shape == 16)
     hipLaunchKernelGGL(mfma_stream<16>, dim3(grid), dim3(256), 0, (hipStream_t)stream, out, iters);
+  else
+    hipLaunchKernelGGL(mfma_stream<4>, dim3(grid), dim3(256), 0, (hipStream_t)stream, out, iters);
+  return hipGetLastError() == hipSuccess ? 0 : -4;
+}
+
+PEAKS_EXPORT int peaks_mfma_chains(float *out, int chains, int iters, int grid, void *stream) {
+  if (!out || iters < 1 || grid < 1) return -1;
+  (void)hipGetLastError();
+  switch (chains) {
+    case 1: hipLaunchKernelGGL(mfma_chains<1>, dim3(grid), dim3(256), 0, (hipStream_t)stream, out, iters); break;
+    case 2: hipLaunchKernelGGL(mfma_chains<2>, dim3(grid), dim3(256), 0, (hipStream_t)stream, out, iters); break;
+    case 4: hipLaunchKernelGGL(mfma_chains<4>, dim3(grid), dim3(256), 0, (hipStream_t)stream, out, iters); break;
+    case 8: hipLaunchKernelGGL(mfma_chains<8>, dim3(grid), dim3(256), 0, (hipStream_t)stream, out, iters); break;
+    default: return -1;
+  }
   return hipGetLastError() == hipSuccess ? 0 : -4;
 }
 
