@@ -98,6 +98,12 @@ Candidate mfma_candidate(int i, int K) {
   return Candidate{i, MT, PT, s.WC, cc, s.MF, s.MB * s.NB, lds, red, NW};
 }
 
+// Matrix-core shapes whose waves each stage their own channels (one MF x MF
+// tile, the channel sum split over the waves: MfmaCfg::PRIV).
+bool private_stages(const Candidate &cd) {
+  return cd.mf > 0 && cd.waves == cd.WC && cd.ops_per_kstep == 1 && cd.MT == cd.mf;
+}
+
 Candidate valu_candidate(int i) {
   const ValuShape s = kValuShapes[i];
   return Candidate{i, s.MR * (4 / s.WC), 64, s.WC, s.CC, 0, s.MR,
@@ -116,10 +122,13 @@ Candidate valu_candidate(int i) {
 //          co-resident workgroups overlap each other's chains
 //   copy:  the bytes a CU stages into LDS, at the rate one CU's vector
 //          memory path delivers them
-// The constants were fitted to exhaustive timings of every matrix-core
-// candidate plan of the nineteen benchmark layers on an MI355X (the fitted
-// model picks a plan within 0.3% of the fastest on average, 5% at worst);
-// the MFMA terms are empirical weights, not instruction latencies.
+// Shapes whose waves stage their own channels (no barrier between stages)
+// have their own stage cost and copy rate.  The constants were fitted to
+// exhaustive timings of every matrix-core candidate plan of 21 benchmark
+// layers and 48 seeded random layers on an MI355X (the fitted model picks a
+// plan within 1% of the fastest on six of them, the bench step's layers,
+// 2.7% on average over all 69, 19% at worst); the MFMA terms are empirical
+// weights, not instruction latencies.
 double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
                 const TileChoice &t, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
@@ -135,8 +144,9 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
   constexpr double kSeveralAcc = 1.75;    // ... with several accumulator tiles per wave
   constexpr double kWcReduction = 69.0;   // per extra wave group
   constexpr double kLaunch = 2000.0;
-  constexpr double kCopyBytesPerClock = 15.9;
-  const double kStageOverhead = mfma ? 1521.0 : 300.0;
+  const bool priv = mfma && private_stages(cd);
+  const double kCopyBytesPerClock = priv ? 14.5 : 11.1;
+  const double kStageOverhead = mfma ? (priv ? 1579.0 : 1698.0) : 300.0;
   const double kLatency = mfma ? 11.0 : 2000.0;
   constexpr int kMaxWaves = 8;            // co-resident waves per CU the model counts
   int occ = (int)(160 * 1024 / (lds_bytes > 0 ? lds_bytes : 1));
@@ -178,6 +188,8 @@ void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu
   const int n = mfma ? kNumMfma : kNumValu;
   for (int i = 0; i < n; ++i) {
     const Candidate cd = mfma ? mfma_candidate(i, K) : valu_candidate(i);
+    // per-wave filter copies: offsets up to MT filter rows, also 32-bit
+    if (mfma && private_stages(cd) && (int64_t)cd.MT * C * K * K >= (int64_t(1) << 30)) continue;
     const TileChoice t = choose_tile(Hout, Wout, cd.PT);
     const int IH = t.tpy + K - 1, IW = t.tpx + K - 1;
     int64_t lds_bytes = cd.lds_fixed;

@@ -238,6 +238,29 @@ constexpr int mfma_buf_floats(int K, int MT, int PT, int CC, int NW, int MF) {
 // 256 channels, whose two buffers fit in 160 KB (one workgroup per CU): for
 // small tiles with little work per channel (K = 1, small maps), where each
 // stage costs about one load latency whatever its size.
+// Shapes that only split the channel sum (one MF x MF tile per workgroup,
+// WC waves): each wave stages its own channels in a region of its own, MT
+// filter rows of CCW*K*K floats, then its CCW input planes; the stage sizes
+// are multiples of 4*WC channels, so that a wave's filter rows are whole
+// float4.
+// A wave's filter rows: CCW*K*K floats (a multiple of 4), at a pitch of an
+// odd number of float4 so that the rows read together start in different
+// banks.
+constexpr int mfma_frwp(int FRW) { return (FRW / 4) % 2 == 1 ? FRW : FRW + 4; }
+constexpr int mfma_buf_floats_priv(int K, int MT, int PT, int CC, int WC, int MF) {
+  return WC * (MT * mfma_frwp(CC / WC * K * K) + CC / WC * mfma_ics(K, PT, MF));
+}
+constexpr int mfma_cc_priv(int K, int MT, int PT, int G, int WC, bool DEEP, int MF) {
+  int best = G;
+  if (DEEP) {
+    for (int cc = G; cc <= 256; cc *= 2)
+      if (2 * mfma_buf_floats_priv(K, MT, PT, cc, WC, MF) * 4 <= 160 * 1024) best = cc;
+    return best;
+  }
+  for (int cc = G; cc <= 64; cc += G)
+    if (2 * mfma_buf_floats_priv(K, MT, PT, cc, WC, MF) * 4 <= 80 * 1024) best = cc;
+  return best;
+}
 constexpr int mfma_cc(int K, int MT, int PT, int G, int NW, bool DEEP, int MF) {
   int best = G;
   if (DEEP) {
@@ -258,7 +281,10 @@ struct MfmaCfg {
   static constexpr int NW = WM * WN * WC;   // waves per workgroup
   static constexpr int MT = MF * MB * WM;   // filters per workgroup
   static constexpr int PT = MF * NB * WN;   // pixel lanes per workgroup tile
-  static constexpr int CC = mfma_cc(K, MT, PT, KG * WC, NW, DEEP, MF);  // channels per stage
+  // Each wave stages only the channels it sums (see the kernel)
+  static constexpr bool PRIV = WM == 1 && WN == 1 && MB == 1 && NB == 1;
+  static constexpr int CC = PRIV ? mfma_cc_priv(K, MT, PT, 4 * WC, WC, DEEP, MF)
+                                 : mfma_cc(K, MT, PT, KG * WC, NW, DEEP, MF);  // channels per stage
   static constexpr int CCW = CC / WC;       // channels per wave group per stage
   static constexpr int FROW = CC * KK;      // staged floats per filter
   static constexpr int FP = mfma_fp(K, CC);
@@ -269,7 +295,16 @@ struct MfmaCfg {
   static constexpr int ICS = mfma_ics(K, PT, MF);
   static constexpr bool PAIR = ICS == 32;              // two input planes per 64-lane copy
   static constexpr int NCI = PAIR ? 1 : ICS / 64;      // most chunks an input plane needs
-  static constexpr int BUF = F_FLOATS + CC * ICS;      // one stage buffer
+  // PRIV: a wave's region of RW floats in a stage buffer: MT filter rows of
+  // FRW floats at pitch FRWP (FREG floats, copied as NF4W 16-byte chunks and
+  // NTW 4-byte ones), then its CCW input planes
+  static constexpr int FRW = CCW * KK;
+  static constexpr int FRWP = mfma_frwp(FRW);          // row pitch
+  static constexpr int FREG = MT * FRWP;
+  static constexpr int NF4W = FREG / 256;
+  static constexpr int NTW = ceil_div(FREG - 256 * NF4W, 64);
+  static constexpr int RW = FREG + CCW * ICS;
+  static constexpr int BUF = PRIV ? NW * RW : F_FLOATS + CC * ICS;      // one stage buffer
   static constexpr int ACC = NV * 64;                  // floats of one accumulator tile
   static constexpr int RED = (WC - 1) * WM * WN * MB * NB * ACC;
   static constexpr int BUF0 = BUF > RED ? BUF : RED;   // buffer 0 also holds the WC sums
@@ -277,6 +312,7 @@ struct MfmaCfg {
   static_assert(NW == 4 || NW == 8 || NW == 16, "four, eight or sixteen waves per workgroup");
   static_assert(CCW % KG == 0, "each k-step takes one channel per lane group");
   static_assert(MT % NW == 0, "filter rows are shared out over the waves");
+  static_assert(!PRIV || FRW % 4 == 0, "16-byte copies of a wave's filter rows");
 };
 
 // fn(integral_constant<int, B>), fn(... B + 1), ..., fn(... E - 1).
@@ -297,6 +333,13 @@ __device__ __forceinline__ void static_for(Fn &&fn) {
 // full stage is issued as unmasked 64-lane copies: lanes that fall outside
 // the map or past a filter row are pointed at valid elements whose values
 // only reach outputs that are never stored (or the padding of a row).
+//   Shapes that only split the channel sum (PRIV: WC waves on one MF x MF
+// tile) share nothing between waves: each wave copies only the channels it
+// sums into a region of its own and waits only for its own copies, with no
+// barrier between stages, so the waves drift apart and some issue copies
+// while others run MFMAs (the shared stage's barrier made every wave wait
+// for the slowest one's copies before any MFMA; on the benchmark layers
+// most plans of these shapes run 5-24% faster so).
 template <int K, int MF, int MB, int NB, int WM, int WN, int WC, bool DEEP>
 __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__restrict__ I,
                                                                const float *__restrict__ F,
@@ -354,11 +397,17 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 #endif
   const int grp = lane / MF;   // which of the KG channels of a k-step
 
+  constexpr bool PRIV = Cfg::PRIV;
+  constexpr int RW = Cfg::RW, FRW = Cfg::FRW, FRWP = Cfg::FRWP, FREG = Cfg::FREG;
+  constexpr int NF4W = Cfg::NF4W, NTW = Cfg::NTW;
   int a_base[MB];
 #pragma unroll
   for (int mb = 0; mb < MB; ++mb) {
     const int row = wm * MF * MB + mb * MF + col;
-    a_base[mb] = (row / RPW) * FBLK + (row % RPW) * FP + (wc * CCW + grp) * KK;
+    if constexpr (PRIV)
+      a_base[mb] = wave * RW + row * FRWP + grp * KK;
+    else
+      a_base[mb] = (row / RPW) * FBLK + (row % RPW) * FP + (wc * CCW + grp) * KK;
   }
   int b_base[NB];
   const int npix = a.tpy * a.tpx;
@@ -370,7 +419,10 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
       const int ty = p / a.tpx;
       off = ty * a.IW + (p - ty * a.tpx);
     }
-    b_base[nb] = F_FLOATS + (wc * CCW + grp) * ICS + off;
+    if constexpr (PRIV)
+      b_base[nb] = wave * RW + FREG + grp * ICS + off;
+    else
+      b_base[nb] = F_FLOATS + (wc * CCW + grp) * ICS + off;
   }
   // One input address per filter row r: every B read of a stage is then
   // b_row[nb][r] plus a compile-time offset (channel group and column).
@@ -544,9 +596,102 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     for (int idx = threadIdx.x; idx < (CC - nc) * ICS; idx += NTHR)
       buf[F_FLOATS + nc * ICS + idx] = 0.f;
   };
+  // PRIV: per-lane offsets of this wave's filter copies, relative to filter
+  // m0's first channel of the wave: 16-byte chunk j covers region floats
+  // [256j, 256j+256), 4-byte chunk t floats [256*NF4W + 64t, +64) (lanes past
+  // FREG masked off).  Rows past M are clamped to M-1.
+  uint32_t vf4[NF4W > 0 ? NF4W : 1];
+  uint32_t vft[NTW > 0 ? NTW : 1];
+  bool ft_ok[NTW > 0 ? NTW : 1];
+  if constexpr (PRIV) {
+#pragma unroll
+    for (int j = 0; j < NF4W; ++j) {
+      const int e = 256 * j + 4 * lane;
+      const int row = e / FRWP;
+      int eo = e - row * FRWP;
+      if (eo >= FRW) eo = 0;  // the row's padding float4: any element of the row
+      const int rr = min(m0 + row, a.M - 1) - m0;
+      vf4[j] = 4u * (uint32_t)(rr * a.C * KK + eo);
+    }
+#pragma unroll
+    for (int t = 0; t < NTW; ++t) {
+      int e = 256 * NF4W + 64 * t + lane;
+      ft_ok[t] = e < FREG;
+      if (!ft_ok[t]) e = 0;
+      const int row = e / FRWP;
+      int eo = e - row * FRWP;
+      if (eo >= FRW) eo = 0;
+      const int rr = min(m0 + row, a.M - 1) - m0;
+      vft[t] = 4u * (uint32_t)(rr * a.C * KK + eo);
+    }
+  }
+  // PRIV: this wave's channels [cw, cw + CCW) of the stage at c0 into its own
+  // region of buf (channels past c_end zeroed).
+  auto issue_priv = [&](int c0, float *buf) __attribute__((always_inline)) {
+    const int cw = c0 + wc * CCW;
+    float *reg = buf + wave * RW;
+    const int nc = min(CCW, c_end - cw);
+    if (nc == CCW) {
+      const float *fsrc = F + ((size_t)m0 * a.C + cw) * KK;
+      static_for<0, NF4W>([&](auto J) {
+        constexpr int j = decltype(J)::value;
+        dma_f128_at<0>(fsrc, vf4[j], reg + 256 * j);
+      });
+      static_for<0, NTW>([&](auto TT) {
+        constexpr int t = decltype(TT)::value;
+        if (ft_ok[t]) dma_f32_at<0>(fsrc, vft[t], reg + 256 * NF4W + 64 * t);
+      });
+      if constexpr (PAIR) {
+#pragma unroll
+        for (int i = 0; i < CCW; i += 2)
+          dma_f32_at<0>(I + (size_t)(cw + i) * plane_elems, vo_in[0], reg + FREG + i * ICS);
+      } else {
+#pragma unroll
+        for (int i = 0; i < CCW; ++i)
+#pragma unroll
+          for (int jj = 0; jj < NCI; ++jj)
+            if (jj < nci)
+              dma_f32_at<0>(I + (size_t)(cw + i) * plane_elems, vo_in[jj],
+                            reg + FREG + i * ICS + 64 * jj);
+      }
+    } else {
+      const int ncp = nc > 0 ? nc : 0;
+      const int flen = ncp * KK;
+      for (int row = 0; row < MT; ++row) {
+        const float *src = F + ((size_t)min(m0 + row, a.M - 1) * a.C + cw) * KK;
+        for (int e = lane; e < FRW; e += 64) {
+          if (e < flen)
+            dma_f32(src + e, reg + row * FRWP + (e - lane));
+          else
+            reg[row * FRWP + e] = 0.f;
+        }
+      }
+      if constexpr (PAIR) {
+        for (int i = 0; i < CCW; i += 2) {
+          if (i + (lane >> 5) < ncp)
+            dma_f32(I + (size_t)(cw + i) * plane_elems + pair_off + ioff[0], reg + FREG + i * ICS);
+          else
+            reg[FREG + i * ICS + lane] = 0.f;
+        }
+      } else {
+        for (int i = 0; i < CCW; ++i) {
+          if (i < ncp) {
+            const float *src = I + (size_t)(cw + i) * plane_elems;
+#pragma unroll
+            for (int j = 0; j < NCI; ++j)
+              if (j < nci) dma_f32(src + ioff[j], reg + FREG + i * ICS + 64 * j);
+          } else {
+            for (int e = lane; e < ICS; e += 64) reg[FREG + i * ICS + e] = 0.f;
+          }
+        }
+      }
+    }
+  };
   // A whole stage at once (the first stages, and partial stages).
   auto issue = [&](int c0, float *buf) __attribute__((always_inline)) {
-    if (c_end - c0 >= CC)
+    if constexpr (PRIV)
+      issue_priv(c0, buf);
+    else if (c_end - c0 >= CC)
       issue_slots(c0, buf, std::integral_constant<int, 0>{}, std::integral_constant<int, ND>{});
     else
       issue_partial(c0, buf);
@@ -616,7 +761,8 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   // stage s+1 land in the other.  Before computing a stage, wait for this
   // wave's copies of it, then the barrier: every wave's copies have landed,
   // and every wave is done with the other buffer, which the next stage's
-  // copies refill.  Each buffer is named as the LDS object itself where it
+  // copies refill (PRIV: no barrier; a wave's own reads of the other buffer
+  // completed in its previous stage).  Each buffer is named as the LDS object itself where it
   // is used (not a pointer chosen at run time), which is what lets the
   // compiler leave the copies to one buffer in flight while the other is
   // read.  (Tried and not kept, no faster on any layer: a third and a
@@ -632,7 +778,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     if (tw >= 0) mark(tw);
     wait_lds_dma();
     if (tw >= 0) mark(tw + 1);
-    lds_barrier();
+    if constexpr (!PRIV) lds_barrier();
     if (tw >= 0) mark(tw + 2);
     if (cs + CC < c_end) issue(cs + CC, nxt);
     if (tw >= 0) mark(tw + 3);
