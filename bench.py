@@ -1067,7 +1067,10 @@ def stage_trace(workload, warmup, report_out=None):
                  "wave of every workgroup; medians over workgroups and stages, in clocks (the "
                  "trace's own stores add a little to each phase).  Per stage: wait = this wave's "
                  "copies of the stage landing, barrier = every wave arriving, issue = issuing "
-                 "the next stage's copies, MFMAs = the stage's matrix instructions.  Setup = "
+                 "the next stage's copies, MFMAs = the stage's matrix instructions (plans whose "
+                 "waves stage their own channels, `w` equal to the wave count: no barrier, and "
+                 "the copies are issued halfway through the MFMAs, so the MFMA phase holds "
+                 "them).  Setup = "
                  "kernel start to the first copies; first copies = issuing stage 0; span = "
                  "kernel start to end of wave 0 (wall clock).", "",
                  "| workload | plan | workgroups | stages | clock GHz | setup | first copies | "

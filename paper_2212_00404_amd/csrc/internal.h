@@ -42,7 +42,9 @@ __device__ __forceinline__ void poison_lds(T *p, int n) {
 // stage's copies, [3] after them, [4] after the stage loop (and channel-group
 // sum), [5] end (wall clock), then for stage s < kStageTraceStages the shader
 // clock at [6 + 5s + i]: i = 0 stage start, 1 after the copy wait, 2 after
-// the barrier, 3 after issuing the next stage's copies, 4 after the MFMAs.
+// the barrier, 3 after issuing the next stage's copies, 4 after the MFMAs
+// (shapes whose waves stage their own channels pass no barrier and issue
+// the next stage's copies halfway through the MFMAs, between marks 3 and 4).
 // Ordinary builds: none of this.
 constexpr int kStageTraceStages = 64;
 constexpr int kStageTraceWords = 6 + 5 * kStageTraceStages;

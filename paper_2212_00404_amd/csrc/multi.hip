@@ -98,11 +98,10 @@ Candidate mfma_candidate(int i, int K) {
   return Candidate{i, MT, PT, s.WC, cc, s.MF, s.MB * s.NB, lds, red, NW};
 }
 
-// Matrix-core shapes whose waves each stage their own channels (one MF x MF
-// tile, the channel sum split over the waves: MfmaCfg::PRIV).
-bool private_stages(const Candidate &cd) {
-  return cd.mf > 0 && cd.waves == cd.WC && cd.ops_per_kstep == 1 && cd.MT == cd.mf;
-}
+// Matrix-core shapes whose waves each stage their own channels (every wave
+// covers the whole tile, the channel sum split over the waves:
+// MfmaCfg::PRIV).
+bool private_stages(const Candidate &cd) { return cd.mf > 0 && cd.waves == cd.WC; }
 
 Candidate valu_candidate(int i) {
   const ValuShape s = kValuShapes[i];
@@ -126,9 +125,10 @@ Candidate valu_candidate(int i) {
 // have their own stage cost and copy rate.  The constants were fitted to
 // exhaustive timings of every matrix-core candidate plan of 21 benchmark
 // layers and 48 seeded random layers on an MI355X (the fitted model picks a
-// plan within 1% of the fastest on six of them, the bench step's layers,
-// 2.7% on average over all 69, 19% at worst); the MFMA terms are empirical
-// weights, not instruction latencies.
+// plan within 4% of the fastest on six of them, the bench step's layers,
+// 3.2% on average over all 69, 20% at worst; a factor for several
+// accumulator tiles per wave fitted to 1 and was dropped); the MFMA terms are
+// empirical weights, not instruction latencies.
 double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
                 const TileChoice &t, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
@@ -141,12 +141,11 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
   constexpr double kMfma32Cycles = 64.3;  // one 32x32x2 MFMA per wave (issue: 64)
   constexpr double kMfma16Cycles = 18.0;  // one 16x16x4 MFMA per wave (issue: 32)
   constexpr double kOneWavePerSimd = 1.25; // MFMA cycles factor with one wave per SIMD
-  constexpr double kSeveralAcc = 1.75;    // ... with several accumulator tiles per wave
   constexpr double kWcReduction = 69.0;   // per extra wave group
   constexpr double kLaunch = 2000.0;
   const bool priv = mfma && private_stages(cd);
-  const double kCopyBytesPerClock = priv ? 14.5 : 11.1;
-  const double kStageOverhead = mfma ? (priv ? 1579.0 : 1698.0) : 300.0;
+  const double kCopyBytesPerClock = priv ? 14.1 : 11.0;
+  const double kStageOverhead = mfma ? (priv ? 1610.0 : 1681.0) : 300.0;
   const double kLatency = mfma ? 11.0 : 2000.0;
   constexpr int kMaxWaves = 8;            // co-resident waves per CU the model counts
   int occ = (int)(160 * 1024 / (lds_bytes > 0 ? lds_bytes : 1));
@@ -159,8 +158,7 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
   const double mcyc = cd.mf == 16 ? kMfma16Cycles : kMfma32Cycles;
   const double per_stage =
       (mfma ? (double)(cd.CC / cd.WC / kg) * kk * cd.ops_per_kstep * mcyc * cd.waves / 4 *
-                  (waves_per_simd < 2 ? kOneWavePerSimd : 1.0) *
-                  (cd.ops_per_kstep > 1 ? kSeveralAcc : 1.0)
+                  (waves_per_simd < 2 ? kOneWavePerSimd : 1.0)
             : (double)(cd.CC / cd.WC) * kk * cd.ops_per_kstep * 4.0) +
       kStageOverhead;
   const double work = (double)per_cu * stages * per_stage;

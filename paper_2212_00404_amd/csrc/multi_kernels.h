@@ -238,7 +238,7 @@ constexpr int mfma_buf_floats(int K, int MT, int PT, int CC, int NW, int MF) {
 // 256 channels, whose two buffers fit in 160 KB (one workgroup per CU): for
 // small tiles with little work per channel (K = 1, small maps), where each
 // stage costs about one load latency whatever its size.
-// Shapes that only split the channel sum (one MF x MF tile per workgroup,
+// Shapes that only split the channel sum (every wave covers the whole tile,
 // WC waves): each wave stages its own channels in a region of its own, MT
 // filter rows of CCW*K*K floats, then its CCW input planes; the stage sizes
 // are multiples of 4*WC channels, so that a wave's filter rows are whole
@@ -282,7 +282,7 @@ struct MfmaCfg {
   static constexpr int MT = MF * MB * WM;   // filters per workgroup
   static constexpr int PT = MF * NB * WN;   // pixel lanes per workgroup tile
   // Each wave stages only the channels it sums (see the kernel)
-  static constexpr bool PRIV = WM == 1 && WN == 1 && MB == 1 && NB == 1;
+  static constexpr bool PRIV = WM == 1 && WN == 1;
   static constexpr int CC = PRIV ? mfma_cc_priv(K, MT, PT, 4 * WC, WC, DEEP, MF)
                                  : mfma_cc(K, MT, PT, KG * WC, NW, DEEP, MF);  // channels per stage
   static constexpr int CCW = CC / WC;       // channels per wave group per stage
@@ -333,13 +333,15 @@ __device__ __forceinline__ void static_for(Fn &&fn) {
 // full stage is issued as unmasked 64-lane copies: lanes that fall outside
 // the map or past a filter row are pointed at valid elements whose values
 // only reach outputs that are never stored (or the padding of a row).
-//   Shapes that only split the channel sum (PRIV: WC waves on one MF x MF
-// tile) share nothing between waves: each wave copies only the channels it
-// sums into a region of its own and waits only for its own copies, with no
-// barrier between stages, so the waves drift apart and some issue copies
-// while others run MFMAs (the shared stage's barrier made every wave wait
-// for the slowest one's copies before any MFMA; on the benchmark layers
-// most plans of these shapes run 5-24% faster so).
+//   Shapes that only split the channel sum (PRIV: WC waves each covering
+// the whole tile) share nothing between waves: each wave copies only the
+// channels it sums into a region of its own and waits only for its own
+// copies, with no barrier between stages, so the waves drift apart and some
+// issue copies while others run MFMAs (the shared stage's barrier made
+// every wave wait for the slowest one's copies before any MFMA; on the
+// benchmark layers most plans of these shapes run 5-30% faster so).  Such a
+// wave issues the next stage's copies halfway through the current stage's
+// MFMAs, not before them (a further 2% on average).
 template <int K, int MF, int MB, int NB, int WM, int WN, int WC, bool DEEP>
 __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__restrict__ I,
                                                                const float *__restrict__ F,
@@ -703,7 +705,8 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   // keep the compiler from hoisting every LDS read of the stage into
   // registers.  (Issuing the next stage's copies a few at a time between
   // these chunks instead of all before them measured 3-13% slower.)
-  auto compute = [&](const float *buf) __attribute__((always_inline)) {
+  // `mid` runs halfway through the chunks (the private stages' copies).
+  auto compute = [&](const float *buf, auto &&mid) __attribute__((always_inline)) {
     constexpr int NQ = (CCW / KG) * KK;
     constexpr int L = 4;
     constexpr int NCH = (NQ + L - 1) / L;
@@ -728,6 +731,11 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
       // chunk's MFMAs: late enough that waiting for them at the start of the
       // next chunk costs nothing, early enough to be in flight for half a
       // chunk.  Scheduling barriers keep the order.
+      if constexpr (ch == NCH / 2) {
+        __builtin_amdgcn_sched_barrier(0);
+        mid();
+        __builtin_amdgcn_sched_barrier(0);
+      }
 #pragma unroll
       for (int l = 0; l < L; ++l) {
         if (l == L / 2) {
@@ -780,9 +788,14 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     if (tw >= 0) mark(tw + 1);
     if constexpr (!PRIV) lds_barrier();
     if (tw >= 0) mark(tw + 2);
-    if (cs + CC < c_end) issue(cs + CC, nxt);
-    if (tw >= 0) mark(tw + 3);
-    compute(cur);
+    if constexpr (PRIV) {
+      if (tw >= 0) mark(tw + 3);
+      compute(cur, [&]() { if (cs + CC < c_end) issue(cs + CC, nxt); });
+    } else {
+      if (cs + CC < c_end) issue(cs + CC, nxt);
+      if (tw >= 0) mark(tw + 3);
+      compute(cur, []() {});
+    }
     if (tw >= 0) mark(tw + 4);
   };
   mark(2);
