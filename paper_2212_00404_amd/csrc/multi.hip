@@ -186,8 +186,12 @@ void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu
   const int n = mfma ? kNumMfma : kNumValu;
   for (int i = 0; i < n; ++i) {
     const Candidate cd = mfma ? mfma_candidate(i, K) : valu_candidate(i);
-    // per-wave filter copies: offsets up to MT filter rows, also 32-bit
-    if (mfma && private_stages(cd) && (int64_t)cd.MT * C * K * K >= (int64_t(1) << 30)) continue;
+    // per-wave copies: filter offsets span MT filter rows, input offsets a
+    // wave's CC/WC planes; both are 32-bit
+    if (mfma && private_stages(cd) &&
+        ((int64_t)cd.MT * C * K * K >= (int64_t(1) << 30) ||
+         (int64_t)(cd.CC / cd.WC) * Wx * Wy >= (int64_t(1) << 30)))
+      continue;
     const TileChoice t = choose_tile(Hout, Wout, cd.PT);
     const int IH = t.tpy + K - 1, IW = t.tpx + K - 1;
     int64_t lds_bytes = cd.lds_fixed;

@@ -247,8 +247,21 @@ constexpr int mfma_buf_floats(int K, int MT, int PT, int CC, int NW, int MF) {
 // odd number of float4 so that the rows read together start in different
 // banks.
 constexpr int mfma_frwp(int FRW) { return (FRW / 4) % 2 == 1 ? FRW : FRW + 4; }
+// The input part of a wave's region (PRIV): CCW planes of ICS floats, then
+// room for the reads of never-stored pixels past the last plane (PT + 4
+// floats; see the kernel).  Two planes per 64-lane copy (32-float planes)
+// take no 16-byte copies and need no room.
+constexpr int mfma_inreg(int K, int PT, int MF, int CCW) {
+  const int ics = mfma_ics(K, PT, MF);
+  return ics == 32 ? CCW * ics : CCW * ics + PT + 4;
+}
+// A wave's whole region, in floats: a multiple of 64 (256 bytes), so that
+// every wave's copies land at the same alignment.
+constexpr int mfma_rw(int K, int MT, int PT, int CCW, int MF) {
+  return (MT * mfma_frwp(CCW * K * K) + mfma_inreg(K, PT, MF, CCW) + 63) / 64 * 64;
+}
 constexpr int mfma_buf_floats_priv(int K, int MT, int PT, int CC, int WC, int MF) {
-  return WC * (MT * mfma_frwp(CC / WC * K * K) + CC / WC * mfma_ics(K, PT, MF));
+  return WC * mfma_rw(K, MT, PT, CC / WC, MF);
 }
 constexpr int mfma_cc_priv(int K, int MT, int PT, int G, int WC, bool DEEP, int MF) {
   int best = G;
@@ -303,7 +316,10 @@ struct MfmaCfg {
   static constexpr int FREG = MT * FRWP;
   static constexpr int NF4W = FREG / 256;
   static constexpr int NTW = ceil_div(FREG - 256 * NF4W, 64);
-  static constexpr int RW = FREG + CCW * ICS;
+  // PRIV input copies: NC4 16-byte chunks, then NT4 4-byte ones (masked)
+  static constexpr int NC4 = CCW * ICS / 256;
+  static constexpr int NT4 = ceil_div(CCW * ICS - 256 * NC4, 64);
+  static constexpr int RW = mfma_rw(K, MT, PT, CCW, MF);
   static constexpr int BUF = PRIV ? NW * RW : F_FLOATS + CC * ICS;      // one stage buffer
   static constexpr int ACC = NV * 64;                  // floats of one accumulator tile
   static constexpr int RED = (WC - 1) * WM * WN * MB * NB * ACC;
@@ -411,6 +427,19 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     else
       a_base[mb] = (row / RPW) * FBLK + (row % RPW) * FP + (wc * CCW + grp) * KK;
   }
+  // PRIV input planes (IN4: where the map is at least one padded row wide
+  // and the tile's padded plane fits the plane stride): rows at pitch IWP
+  // (IW rounded up to 4), copied 16 bytes per lane, staged from map column
+  // sx, the tile's first column moved left so that no 16-byte read leaves
+  // the map (the valid pixels' columns stay inside the staged window;
+  // never-stored pixels may read past it, inside the wave's region).
+  // Otherwise (and on the shared layout) rows at pitch IW from the tile's
+  // first column, copied 4 bytes per lane.
+  constexpr int NC4 = Cfg::NC4, NT4 = Cfg::NT4;
+  const int IWP = (a.IW + 3) & ~3;
+  const bool in4 = PRIV && !PAIR && a.Wx >= IWP && a.IH * IWP <= ICS;
+  const int ipitch = in4 ? IWP : a.IW;
+  const int sx = in4 ? min(px0, a.Wx - IWP) : px0;
   int b_base[NB];
   const int npix = a.tpy * a.tpx;
 #pragma unroll
@@ -419,7 +448,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     int off = 0;  // padding lanes read pixel (0, 0); their results are dropped
     if (p < npix) {
       const int ty = p / a.tpx;
-      off = ty * a.IW + (p - ty * a.tpx);
+      off = ty * ipitch + (p - ty * a.tpx) + (px0 - sx);
     }
     if constexpr (PRIV)
       b_base[nb] = wave * RW + FREG + grp * ICS + off;
@@ -432,7 +461,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-    for (int r = 0; r < K; ++r) b_row[nb][r] = b_base[nb] + r * a.IW;
+    for (int r = 0; r < K; ++r) b_row[nb][r] = b_base[nb] + r * ipitch;
 
   // Per-lane source offsets of one input plane, chunk j covers plane elements
   // [64j, 64j+64): element e is row e / IW, column e % IW of the halo tile,
@@ -627,9 +656,44 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
       vft[t] = 4u * (uint32_t)(rr * a.C * KK + eo);
     }
   }
+  // PRIV, IN4: per-lane offsets of the input copies, relative to the wave's
+  // first channel: 16-byte chunk j covers region floats [256j, 256j+256) of
+  // the CCW planes (plane i at i*ICS, rows at pitch IWP), 4-byte chunk t
+  // floats [256*NC4 + 64t, +64) (lanes past the planes masked off); lanes on
+  // a plane's padding read plane 0's first element.  vpl4/vplt: the lane's
+  // plane.  The planner keeps CCW*Wx*Wy below 2^30.
+  uint32_t vin4[NC4 > 0 ? NC4 : 1], vint[NT4 > 0 ? NT4 : 1];
+  int vpl4[NC4 > 0 ? NC4 : 1], vplt[NT4 > 0 ? NT4 : 1];
+  bool it_ok[NT4 > 0 ? NT4 : 1];
+  auto in_src = [&](int e, uint32_t &vo, int &pl) __attribute__((always_inline)) {
+    int i = e / ICS;
+    const int pe = e - i * ICS;
+    int row = pe / IWP;
+    int cx = pe - row * IWP;
+    if (i >= CCW || row >= a.IH) i = row = cx = 0;
+    const int gy = min(py0 + row, a.Wy - 1);
+    vo = 4u * (uint32_t)((size_t)i * plane_elems + (size_t)gy * a.Wx + sx + cx);
+    pl = i;
+  };
+  if constexpr (PRIV && !PAIR) {
+    if (in4) {
+#pragma unroll
+      for (int j = 0; j < NC4; ++j) in_src(256 * j + 4 * lane, vin4[j], vpl4[j]);
+#pragma unroll
+      for (int t = 0; t < NT4; ++t) {
+        const int e = 256 * NC4 + 64 * t + lane;
+        it_ok[t] = e < CCW * ICS;
+        in_src(it_ok[t] ? e : 0, vint[t], vplt[t]);
+      }
+    }
+  }
   // PRIV: this wave's channels [cw, cw + CCW) of the stage at c0 into its own
   // region of buf (channels past c_end zeroed).
-  auto issue_priv = [&](int c0, float *buf) __attribute__((always_inline)) {
+  // IN4 is the run-time in4 as a compile-time constant: the stage loop is
+  // instantiated once per copy form, so no branch on it sits between the
+  // MFMAs.
+  auto issue_priv = [&](int c0, float *buf, auto IN4) __attribute__((always_inline)) {
+    constexpr bool use4 = decltype(IN4)::value;
     const int cw = c0 + wc * CCW;
     float *reg = buf + wave * RW;
     const int nc = min(CCW, c_end - cw);
@@ -648,13 +712,25 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
         for (int i = 0; i < CCW; i += 2)
           dma_f32_at<0>(I + (size_t)(cw + i) * plane_elems, vo_in[0], reg + FREG + i * ICS);
       } else {
+        if constexpr (use4) {
+          static_for<0, NC4>([&](auto J) {
+            constexpr int j = decltype(J)::value;
+            dma_f128_at<0>(I + (size_t)cw * plane_elems, vin4[j], reg + FREG + 256 * j);
+          });
+          static_for<0, NT4>([&](auto TT) {
+            constexpr int t = decltype(TT)::value;
+            if (it_ok[t])
+              dma_f32_at<0>(I + (size_t)cw * plane_elems, vint[t], reg + FREG + 256 * NC4 + 64 * t);
+          });
+        } else {
 #pragma unroll
-        for (int i = 0; i < CCW; ++i)
+          for (int i = 0; i < CCW; ++i)
 #pragma unroll
-          for (int jj = 0; jj < NCI; ++jj)
-            if (jj < nci)
-              dma_f32_at<0>(I + (size_t)(cw + i) * plane_elems, vo_in[jj],
-                            reg + FREG + i * ICS + 64 * jj);
+            for (int jj = 0; jj < NCI; ++jj)
+              if (jj < nci)
+                dma_f32_at<0>(I + (size_t)(cw + i) * plane_elems, vo_in[jj],
+                              reg + FREG + i * ICS + 64 * jj);
+        }
       }
     } else {
       const int ncp = nc > 0 ? nc : 0;
@@ -675,6 +751,23 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
           else
             reg[FREG + i * ICS + lane] = 0.f;
         }
+      } else if (use4 && ncp > 0) {
+        // planes past the last channel re-read channel cw + ncp - 1: their
+        // filter values are zero, so they add nothing
+        static_for<0, NC4>([&](auto J) {
+          constexpr int j = decltype(J)::value;
+          const int over = vpl4[j] - (ncp - 1);
+          const uint32_t vo =
+              over > 0 ? vin4[j] - 4u * (uint32_t)((size_t)over * plane_elems) : vin4[j];
+          dma_f128_at<0>(I + (size_t)cw * plane_elems, vo, reg + FREG + 256 * j);
+        });
+        static_for<0, NT4>([&](auto TT) {
+          constexpr int t = decltype(TT)::value;
+          const int over = vplt[t] - (ncp - 1);
+          const uint32_t vo =
+              over > 0 ? vint[t] - 4u * (uint32_t)((size_t)over * plane_elems) : vint[t];
+          if (it_ok[t]) dma_f32_at<0>(I + (size_t)cw * plane_elems, vo, reg + FREG + 256 * NC4 + 64 * t);
+        });
       } else {
         for (int i = 0; i < CCW; ++i) {
           if (i < ncp) {
@@ -690,9 +783,9 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     }
   };
   // A whole stage at once (the first stages, and partial stages).
-  auto issue = [&](int c0, float *buf) __attribute__((always_inline)) {
+  auto issue = [&](int c0, float *buf, auto IN4) __attribute__((always_inline)) {
     if constexpr (PRIV)
-      issue_priv(c0, buf);
+      issue_priv(c0, buf, IN4);
     else if (c_end - c0 >= CC)
       issue_slots(c0, buf, std::integral_constant<int, 0>{}, std::integral_constant<int, ND>{});
     else
@@ -777,7 +870,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   // fourth buffer; the copies of stage s+2 spread between the MFMA chunks
   // of stage s over three buffers; waves that only copy beside waves that
   // only compute; a stage order rotated per output tile.)
-  auto stage = [&](auto J, int cs) __attribute__((always_inline)) {
+  auto stage = [&](auto J, int cs, auto IN4) __attribute__((always_inline)) {
     constexpr int j = decltype(J)::value;
     float *cur = j == 0 ? buf0 : buf1;
     float *nxt = j == 0 ? buf1 : buf0;
@@ -790,22 +883,28 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     if (tw >= 0) mark(tw + 2);
     if constexpr (PRIV) {
       if (tw >= 0) mark(tw + 3);
-      compute(cur, [&]() { if (cs + CC < c_end) issue(cs + CC, nxt); });
+      compute(cur, [&]() { if (cs + CC < c_end) issue(cs + CC, nxt, IN4); });
     } else {
-      if (cs + CC < c_end) issue(cs + CC, nxt);
+      if (cs + CC < c_end) issue(cs + CC, nxt, IN4);
       if (tw >= 0) mark(tw + 3);
       compute(cur, []() {});
     }
     if (tw >= 0) mark(tw + 4);
   };
-  mark(2);
-  issue(0, buf0);
-  mark(3);
-  for (int c0 = 0; c0 < c_end; c0 += 2 * CC) {
-    stage(std::integral_constant<int, 0>{}, c0);
-    if (c0 + CC >= c_end) break;
-    stage(std::integral_constant<int, 1>{}, c0 + CC);
-  }
+  auto run_stages = [&](auto IN4) __attribute__((always_inline)) {
+    mark(2);
+    issue(0, buf0, IN4);
+    mark(3);
+    for (int c0 = 0; c0 < c_end; c0 += 2 * CC) {
+      stage(std::integral_constant<int, 0>{}, c0, IN4);
+      if (c0 + CC >= c_end) break;
+      stage(std::integral_constant<int, 1>{}, c0 + CC, IN4);
+    }
+  };
+  if (PRIV && !PAIR && in4)
+    run_stages(std::true_type{});
+  else
+    run_stages(std::false_type{});
 
   // Fixed-order sum of the WC channel groups through LDS: group 0 adds the
   // partial tiles of groups 1, 2, ..., WC-1 in that order.
