@@ -1,5 +1,6 @@
 // Multi-channel direct convolution: the planner (workgroup shape, output
 // tile, channels per stage, time model) and launch_multi (paper, Section 3.2).
+#include <cmath>
 #include <vector>
 
 #include "multi_kernels.h"
@@ -124,12 +125,14 @@ Candidate valu_candidate(int i) {
 // Shapes whose waves stage their own channels (no barrier between stages)
 // have their own stage cost and copy rate.  The constants were fitted to
 // exhaustive timings of every matrix-core candidate plan of 21 benchmark
-// layers and 48 seeded random layers on an MI355X (the fitted model picks a
-// plan within 4% of the fastest on six of them, the bench step's layers,
-// 3.2% on average over all 69, 20% at worst; a factor for several
-// accumulator tiles per wave fitted to 1 and was dropped); the MFMA terms are
-// empirical weights, not instruction latencies.
-double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
+// layers and 48 seeded random layers on an MI355X, the six bench-step
+// layers weighted five times (the fitted model picks the fastest plan on
+// five of those six, 1.14x on the sixth, 2.2% above the fastest on average
+// over all 69, 20% at worst; 2.6% and 17% on 24 other random layers; a
+// factor for several accumulator tiles per wave fitted to 1 and was
+// dropped); the MFMA terms are empirical weights, not instruction
+// latencies.
+double estimate(const Candidate &cd, bool mfma, int C, int M, int Wx, int K, int num_cu,
                 const TileChoice &t, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
   const int64_t mtiles = (M + cd.MT - 1) / cd.MT;
@@ -140,12 +143,18 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
   // eight-wave and deep shapes, the vector kernels on the same layers.
   constexpr double kMfma32Cycles = 64.3;  // one 32x32x2 MFMA per wave (issue: 64)
   constexpr double kMfma16Cycles = 18.0;  // one 16x16x4 MFMA per wave (issue: 32)
-  constexpr double kOneWavePerSimd = 1.25; // MFMA cycles factor with one wave per SIMD
+  constexpr double kOneWavePerSimd = 1.13; // MFMA cycles factor with one wave per SIMD
   constexpr double kWcReduction = 69.0;   // per extra wave group
   constexpr double kLaunch = 2000.0;
+  // Private stages, and among them those whose input planes go 16 bytes per
+  // lane (the kernel's in4 condition), have their own copy rate and stage
+  // cost.
   const bool priv = mfma && private_stages(cd);
-  const double kCopyBytesPerClock = priv ? 14.1 : 11.0;
-  const double kStageOverhead = mfma ? (priv ? 1610.0 : 1681.0) : 300.0;
+  const int ics = priv ? mfma_ics(K, cd.PT, cd.mf) : 0;
+  const int ih = t.tpy + K - 1, iwp = (t.tpx + K - 1 + 3) & ~3;
+  const bool in4 = priv && ics != 32 && Wx >= iwp && ih * iwp <= ics;
+  const double kCopyBytesPerClock = in4 ? 12.1 : priv ? 12.8 : 11.7;
+  const double kStageOverhead = mfma ? (in4 ? 294.0 : priv ? 410.0 : 652.0) : 300.0;
   const double kLatency = mfma ? 11.0 : 2000.0;
   constexpr int kMaxWaves = 8;            // co-resident waves per CU the model counts
   int occ = (int)(160 * 1024 / (lds_bytes > 0 ? lds_bytes : 1));
@@ -168,7 +177,10 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int K, int num_cu,
   // Bytes staged per workgroup: the filter slice and the input halo tile of
   // every channel.
   const double staged = 4.0 * C * ((double)cd.MT * kk + (t.tpy + K - 1.0) * (t.tpx + K - 1.0));
-  const double copy = mfma ? (double)per_cu * staged / kCopyBytesPerClock : 0.0;
+  // the copy rate grows a little with the waves on a CU issuing copies
+  const double wpc = (double)cd.waves * (per_cu < occ ? per_cu : occ);
+  const double copy =
+      mfma ? (double)per_cu * staged / (kCopyBytesPerClock * std::pow(wpc / 8.0, 0.05)) : 0.0;
   double tm = work > chain ? work : chain;
   if (copy > tm) tm = copy;
   return tm + (cd.WC - 1) * kWcReduction + kLatency + kLaunch;
@@ -200,7 +212,7 @@ void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu
       lds_bytes = 4 * (stage > cd.red_floats ? stage : cd.red_floats);
     }
     if (lds_bytes > kMaxLds) continue;
-    const double tm = estimate(cd, mfma, C, M, K, num_cu, t, lds_bytes);
+    const double tm = estimate(cd, mfma, C, M, Wx, K, num_cu, t, lds_bytes);
     MultiPlan p{};
     p.variant = mfma ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
     p.kernel = i;
