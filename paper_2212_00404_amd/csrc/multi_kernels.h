@@ -440,6 +440,9 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   const bool in4 = PRIV && !PAIR && a.Wx >= IWP && a.IH * IWP <= ICS;
   const int ipitch = in4 ? IWP : a.IW;
   const int sx = in4 ? min(px0, a.Wx - IWP) : px0;
+  // Divisions by run-time tile sizes through a float reciprocal (fdiv): the
+  // integer division sequence costs tens of instructions per lane.
+  const float inv_tpx = 1.0f / (float)a.tpx;
   int b_base[NB];
   const int npix = a.tpy * a.tpx;
 #pragma unroll
@@ -447,7 +450,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     const int p = wn * MF * NB + nb * MF + col;
     int off = 0;  // padding lanes read pixel (0, 0); their results are dropped
     if (p < npix) {
-      const int ty = p / a.tpx;
+      const int ty = fdiv(p, a.tpx, inv_tpx);
       off = ty * ipitch + (p - ty * a.tpx) + (px0 - sx);
     }
     if constexpr (PRIV)
@@ -471,11 +474,12 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   const int plane = a.IH * a.IW;
   const int nci = PAIR ? 1 : (plane + 63) >> 6;
   int ioff[NCI];
+  const float inv_iw = 1.0f / (float)a.IW;
 #pragma unroll
   for (int j = 0; j < NCI; ++j) {
     int e = PAIR ? (lane & 31) : 64 * j + lane;
     if (e >= plane) e = 0;
-    const int iy = e / a.IW;
+    const int iy = fdiv(e, a.IW, inv_iw);
     const int gy = min(py0 + iy, a.Wy - 1);
     const int gx = min(px0 + (e - iy * a.IW), a.Wx - 1);
     ioff[j] = gy * a.Wx + gx;
@@ -665,10 +669,11 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   uint32_t vin4[NC4 > 0 ? NC4 : 1], vint[NT4 > 0 ? NT4 : 1];
   int vpl4[NC4 > 0 ? NC4 : 1], vplt[NT4 > 0 ? NT4 : 1];
   bool it_ok[NT4 > 0 ? NT4 : 1];
+  const float inv_iwp = 1.0f / (float)IWP;
   auto in_src = [&](int e, uint32_t &vo, int &pl) __attribute__((always_inline)) {
     int i = e / ICS;
     const int pe = e - i * ICS;
-    int row = pe / IWP;
+    int row = fdiv(pe, IWP, inv_iwp);
     int cx = pe - row * IWP;
     if (i >= CCW || row >= a.IH) i = row = cx = 0;
     const int gy = min(py0 + row, a.Wy - 1);
@@ -943,7 +948,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   for (int nb = 0; nb < NB; ++nb) {
     const int p = wn * MF * NB + nb * MF + col;
     if (p >= npix) continue;
-    const int ty = p / a.tpx;
+    const int ty = fdiv(p, a.tpx, inv_tpx);
     const int gy = py0 + ty;
     const int gx = px0 + (p - ty * a.tpx);
     if (gy >= Hout || gx >= Wout) continue;
