@@ -249,11 +249,9 @@ constexpr int mfma_buf_floats(int K, int MT, int PT, int CC, int NW, int MF) {
 constexpr int mfma_frwp(int FRW) { return (FRW / 4) % 2 == 1 ? FRW : FRW + 4; }
 // The input part of a wave's region (PRIV): CCW planes of ICS floats, then
 // room for the reads of never-stored pixels past the last plane (PT + 4
-// floats; see the kernel).  Two planes per 64-lane copy (32-float planes)
-// take no 16-byte copies and need no room.
+// floats; see the kernel).
 constexpr int mfma_inreg(int K, int PT, int MF, int CCW) {
-  const int ics = mfma_ics(K, PT, MF);
-  return ics == 32 ? CCW * ics : CCW * ics + PT + 4;
+  return CCW * mfma_ics(K, PT, MF) + PT + 4;
 }
 // A wave's whole region, in floats: a multiple of 64 (256 bytes), so that
 // every wave's copies land at the same alignment.
@@ -437,7 +435,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   // first column, copied 4 bytes per lane.
   constexpr int NC4 = Cfg::NC4, NT4 = Cfg::NT4;
   const int IWP = (a.IW + 3) & ~3;
-  const bool in4 = PRIV && !PAIR && a.Wx >= IWP && a.IH * IWP <= ICS;
+  const bool in4 = PRIV && a.Wx >= IWP && a.IH * IWP <= ICS;
   const int ipitch = in4 ? IWP : a.IW;
   const int sx = in4 ? min(px0, a.Wx - IWP) : px0;
   // Divisions by run-time tile sizes through a float reciprocal (fdiv): the
@@ -680,7 +678,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     vo = 4u * (uint32_t)((size_t)i * plane_elems + (size_t)gy * a.Wx + sx + cx);
     pl = i;
   };
-  if constexpr (PRIV && !PAIR) {
+  if constexpr (PRIV) {
     if (in4) {
 #pragma unroll
       for (int j = 0; j < NC4; ++j) in_src(256 * j + 4 * lane, vin4[j], vpl4[j]);
@@ -712,30 +710,28 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
         constexpr int t = decltype(TT)::value;
         if (ft_ok[t]) dma_f32_at<0>(fsrc, vft[t], reg + 256 * NF4W + 64 * t);
       });
-      if constexpr (PAIR) {
+      if constexpr (use4) {
+        static_for<0, NC4>([&](auto J) {
+          constexpr int j = decltype(J)::value;
+          dma_f128_at<0>(I + (size_t)cw * plane_elems, vin4[j], reg + FREG + 256 * j);
+        });
+        static_for<0, NT4>([&](auto TT) {
+          constexpr int t = decltype(TT)::value;
+          if (it_ok[t])
+            dma_f32_at<0>(I + (size_t)cw * plane_elems, vint[t], reg + FREG + 256 * NC4 + 64 * t);
+        });
+      } else if constexpr (PAIR) {
 #pragma unroll
         for (int i = 0; i < CCW; i += 2)
           dma_f32_at<0>(I + (size_t)(cw + i) * plane_elems, vo_in[0], reg + FREG + i * ICS);
       } else {
-        if constexpr (use4) {
-          static_for<0, NC4>([&](auto J) {
-            constexpr int j = decltype(J)::value;
-            dma_f128_at<0>(I + (size_t)cw * plane_elems, vin4[j], reg + FREG + 256 * j);
-          });
-          static_for<0, NT4>([&](auto TT) {
-            constexpr int t = decltype(TT)::value;
-            if (it_ok[t])
-              dma_f32_at<0>(I + (size_t)cw * plane_elems, vint[t], reg + FREG + 256 * NC4 + 64 * t);
-          });
-        } else {
 #pragma unroll
-          for (int i = 0; i < CCW; ++i)
+        for (int i = 0; i < CCW; ++i)
 #pragma unroll
-            for (int jj = 0; jj < NCI; ++jj)
-              if (jj < nci)
-                dma_f32_at<0>(I + (size_t)(cw + i) * plane_elems, vo_in[jj],
-                              reg + FREG + i * ICS + 64 * jj);
-        }
+          for (int jj = 0; jj < NCI; ++jj)
+            if (jj < nci)
+              dma_f32_at<0>(I + (size_t)(cw + i) * plane_elems, vo_in[jj],
+                            reg + FREG + i * ICS + 64 * jj);
       }
     } else {
       const int ncp = nc > 0 ? nc : 0;
@@ -749,14 +745,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
             reg[row * FRWP + e] = 0.f;
         }
       }
-      if constexpr (PAIR) {
-        for (int i = 0; i < CCW; i += 2) {
-          if (i + (lane >> 5) < ncp)
-            dma_f32(I + (size_t)(cw + i) * plane_elems + pair_off + ioff[0], reg + FREG + i * ICS);
-          else
-            reg[FREG + i * ICS + lane] = 0.f;
-        }
-      } else if (use4 && ncp > 0) {
+      if (use4 && ncp > 0) {
         // planes past the last channel re-read channel cw + ncp - 1: their
         // filter values are zero, so they add nothing
         static_for<0, NC4>([&](auto J) {
@@ -773,6 +762,13 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
               over > 0 ? vint[t] - 4u * (uint32_t)((size_t)over * plane_elems) : vint[t];
           if (it_ok[t]) dma_f32_at<0>(I + (size_t)cw * plane_elems, vo, reg + FREG + 256 * NC4 + 64 * t);
         });
+      } else if constexpr (PAIR) {
+        for (int i = 0; i < CCW; i += 2) {
+          if (i + (lane >> 5) < ncp)
+            dma_f32(I + (size_t)(cw + i) * plane_elems + pair_off + ioff[0], reg + FREG + i * ICS);
+          else
+            reg[FREG + i * ICS + lane] = 0.f;
+        }
       } else {
         for (int i = 0; i < CCW; ++i) {
           if (i < ncp) {
@@ -906,7 +902,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
       stage(std::integral_constant<int, 1>{}, c0 + CC, IN4);
     }
   };
-  if (PRIV && !PAIR && in4)
+  if (PRIV && in4)
     run_stages(std::true_type{});
   else
     run_stages(std::false_type{});
