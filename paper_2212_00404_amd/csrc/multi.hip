@@ -199,9 +199,11 @@ void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu
   for (int i = 0; i < n; ++i) {
     const Candidate cd = mfma ? mfma_candidate(i, K) : valu_candidate(i);
     // per-wave copies: filter offsets span MT filter rows, input offsets a
-    // wave's CC/WC planes; both are 32-bit
+    // wave's CC/WC planes; both are 32-bit (and C*K*K goes through a 24-bit
+    // multiply)
     if (mfma && private_stages(cd) &&
-        ((int64_t)cd.MT * C * K * K >= (int64_t(1) << 30) ||
+        ((int64_t)C * K * K >= (int64_t(1) << 24) ||
+         (int64_t)cd.MT * C * K * K >= (int64_t(1) << 30) ||
          (int64_t)(cd.CC / cd.WC) * Wx * Wy >= (int64_t(1) << 30)))
       continue;
     const TileChoice t = choose_tile(Hout, Wout, cd.PT);

@@ -75,6 +75,10 @@ typedef float floatx16 __attribute__((ext_vector_type(16)));
 
 constexpr int kBlock = 256;
 
+// a * b for 0 <= a, b < 2^24 with a product below 2^32: one full-rate
+// 24-bit multiply (a 32-bit one issues at a quarter of the rate).
+__device__ __forceinline__ int mul24(int a, int b) { return (int)__umul24(a, b); }
+
 // n / d for 0 <= n < 2^22 and 1 <= d < 2^11 using a float reciprocal.
 __device__ __forceinline__ int fdiv(int n, int d, float inv) {
   int q = __float2int_rz((float)n * inv);
@@ -437,7 +441,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   // first column, copied 4 bytes per lane.
   constexpr int NC4 = Cfg::NC4, NT4 = Cfg::NT4;
   const int IWP = (a.IW + 3) & ~3;
-  const bool in4 = PRIV && a.Wx >= IWP && a.IH * IWP <= ICS;
+  const bool in4 = PRIV && a.Wx >= IWP && a.IH * IWP <= ICS && a.Wx * a.Wy < (1 << 24);
   const int ipitch = in4 ? IWP : a.IW;
   const int sx = in4 ? min(px0, a.Wx - IWP) : px0;
   // Divisions by run-time tile sizes through a float reciprocal (fdiv): the
@@ -451,7 +455,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
     int off = 0;  // padding lanes read pixel (0, 0); their results are dropped
     if (p < npix) {
       const int ty = fdiv(p, a.tpx, inv_tpx);
-      off = ty * ipitch + (p - ty * a.tpx) + (px0 - sx);
+      off = mul24(ty, ipitch) + (p - mul24(ty, a.tpx)) + (px0 - sx);
     }
     if constexpr (PRIV)
       b_base[nb] = wave * RW + FREG + grp * ICS + off;
@@ -473,16 +477,22 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   // next channel (one map further).
   const int plane = a.IH * a.IW;
   const int nci = PAIR ? 1 : (plane + 63) >> 6;
+  // (Not used by the 16-byte input copies of private stages.)
   int ioff[NCI];
   const float inv_iw = 1.0f / (float)a.IW;
+  if (!in4) {
 #pragma unroll
-  for (int j = 0; j < NCI; ++j) {
-    int e = PAIR ? (lane & 31) : 64 * j + lane;
-    if (e >= plane) e = 0;
-    const int iy = fdiv(e, a.IW, inv_iw);
-    const int gy = min(py0 + iy, a.Wy - 1);
-    const int gx = min(px0 + (e - iy * a.IW), a.Wx - 1);
-    ioff[j] = gy * a.Wx + gx;
+    for (int j = 0; j < NCI; ++j) {
+      int e = PAIR ? (lane & 31) : 64 * j + lane;
+      if (e >= plane) e = 0;
+      const int iy = fdiv(e, a.IW, inv_iw);
+      const int gy = min(py0 + iy, a.Wy - 1);
+      const int gx = min(px0 + (e - iy * a.IW), a.Wx - 1);
+      ioff[j] = gy * a.Wx + gx;
+    }
+  } else {
+#pragma unroll
+    for (int j = 0; j < NCI; ++j) ioff[j] = 0;
   }
   // Filter rows.  Rows of at least 256 floats whose length is a multiple of
   // 4 (F128) start with NF4 16-byte-per-lane copies (1 KB per instruction,
@@ -635,6 +645,8 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   // m0's first channel of the wave: 16-byte chunk j covers region floats
   // [256j, 256j+256), 4-byte chunk t floats [256*NF4W + 64t, +64) (lanes past
   // FREG masked off).  Rows past M are clamped to M-1.
+  // (The planner keeps C*K*K below 2^24 for these shapes.)
+  const int ckk = a.C * KK;
   uint32_t vf4[NF4W > 0 ? NF4W : 1];
   uint32_t vft[NTW > 0 ? NTW : 1];
   bool ft_ok[NTW > 0 ? NTW : 1];
@@ -646,7 +658,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
       int eo = e - row * FRWP;
       if (eo >= FRW) eo = 0;  // the row's padding float4: any element of the row
       const int rr = min(m0 + row, a.M - 1) - m0;
-      vf4[j] = 4u * (uint32_t)(rr * a.C * KK + eo);
+      vf4[j] = 4u * (uint32_t)(mul24(rr, ckk) + eo);
     }
 #pragma unroll
     for (int t = 0; t < NTW; ++t) {
@@ -657,7 +669,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
       int eo = e - row * FRWP;
       if (eo >= FRW) eo = 0;
       const int rr = min(m0 + row, a.M - 1) - m0;
-      vft[t] = 4u * (uint32_t)(rr * a.C * KK + eo);
+      vft[t] = 4u * (uint32_t)(mul24(rr, ckk) + eo);
     }
   }
   // PRIV, IN4: per-lane offsets of the input copies, relative to the wave's
@@ -670,14 +682,15 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   int vpl4[NC4 > 0 ? NC4 : 1], vplt[NT4 > 0 ? NT4 : 1];
   bool it_ok[NT4 > 0 ? NT4 : 1];
   const float inv_iwp = 1.0f / (float)IWP;
+  const int plane_i = a.Wx * a.Wy;   // below 2^24 where IN4 holds
   auto in_src = [&](int e, uint32_t &vo, int &pl) __attribute__((always_inline)) {
     int i = e / ICS;
     const int pe = e - i * ICS;
     int row = fdiv(pe, IWP, inv_iwp);
-    int cx = pe - row * IWP;
+    int cx = pe - mul24(row, IWP);
     if (i >= CCW || row >= a.IH) i = row = cx = 0;
     const int gy = min(py0 + row, a.Wy - 1);
-    vo = 4u * (uint32_t)((size_t)i * plane_elems + (size_t)gy * a.Wx + sx + cx);
+    vo = 4u * (uint32_t)(mul24(i, plane_i) + mul24(gy, a.Wx) + sx + cx);
     pl = i;
   };
   if constexpr (PRIV) {
