@@ -350,9 +350,10 @@ __device__ __forceinline__ void static_for(Fn &&fn) {
 // filter slice and input tile of stage s+1 stream into the other buffer with
 // direct global->LDS loads (no registers, no LDS write instructions).  The
 // per-lane source offsets of a stage are fixed for the whole kernel, so a
-// full stage is issued as unmasked 64-lane copies: lanes that fall outside
-// the map or past a filter row are pointed at valid elements whose values
-// only reach outputs that are never stored (or the padding of a row).
+// full stage of the shared layout is issued as unmasked 64-lane copies:
+// lanes that fall outside the map or past a filter row are pointed at valid
+// elements whose values only reach outputs that are never stored (or the
+// padding of a row); the private layout below masks its 4-byte tail chunks.
 //   Shapes that only split the channel sum (PRIV: WC waves each covering
 // the whole tile) share nothing between waves: each wave copies only the
 // channels it sums into a region of its own and waits only for its own
@@ -1141,6 +1142,7 @@ constexpr MfmaShape kMfmaShapes[] = {
     {16, 1, 1, 1, 1, 4, false},  // 16 x 16, four waves splitting the channel sum
     {16, 1, 1, 2, 1, 4, false},  // 32 x 16, eight waves (four per 16 filters)
     {16, 1, 1, 1, 2, 4, false},  // 16 x 32, eight waves (four per 16 pixels)
+    {16, 1, 2, 1, 1, 8, false},  // 16 x 32, eight waves splitting the channel sum
 };
 constexpr int kNumMfma = sizeof(kMfmaShapes) / sizeof(kMfmaShapes[0]);
 
