@@ -214,6 +214,48 @@ def test_wave_split_test_shapes_split_inside_the_workgroup():
     assert sum(dc.plan_multi(*s)["waves_c"] > 1 for s in split_shapes.REUSE) >= 3
 
 
+def test_private_layers_reach_every_copy_form():
+    """The layers of the private-stage GPU test still reach each copy form.
+    The form a plan takes follows the kernel's rule: a plan is privately
+    staged when every wave covers the whole tile (block / 64 == waves_c); its
+    input planes go 16 bytes per lane when the map is at least one padded row
+    (IW rounded up to 4) wide and the padded plane fits the plane slot
+    (64 * ceil(K * (PT + K - 1) / 64), +16 for 16-wide instructions; 32 where a
+    32-pixel tile's plane fits 32 floats), PT being the shape's pixels per
+    tile."""
+    from private_layers import PRIVATE_LAYERS
+    pt = {5: 64, 8: 32, 9: 32, 10: 16, 11: 16, 12: 16, 15: 32}   # private shapes
+    seen = set()
+    for C, M, Wx, Wy, K in PRIVATE_LAYERS:
+        for p in dc.plan_multi_candidates(C, M, Wx, Wy, K, "mfma"):
+            if p["block"] // 64 != p["waves_c"]:
+                continue
+            mf = 32 if p["kernel"] in (5, 8, 9) else 16
+            PT = pt[p["kernel"]]
+            ics = 32 if mf == 32 and K * (PT + K - 1) <= 32 else \
+                64 * -(-K * (PT + K - 1) // 64) + (16 if mf == 16 else 0)
+            iw, ih = p["tile_w"] + K - 1, p["tile_h"] + K - 1
+            iwp = (iw + 3) // 4 * 4
+            in4 = Wx >= iwp and ih * iwp <= ics
+            tx = -(-(Wx - K + 1) // p["tile_w"])
+            rem = C % p["chunk_c"]
+            idle = rem != 0 and rem <= (p["waves_c"] - 1) * (p["chunk_c"] // p["waves_c"])
+            seen |= {"in4" if in4 else "fallback"}
+            if in4 and ics == 32:
+                seen.add("in4 paired planes")
+            if in4 and (tx - 1) * p["tile_w"] + iwp > Wx:
+                seen.add("in4 window moved left")
+            if idle:
+                seen.add("in4 idle waves" if in4 else "fallback idle waves")
+            if p["kernel"] == 15:
+                seen.add("16 x 32 eight waves")
+            if K % 2 == 0:
+                seen.add("even K")
+    assert seen >= {"in4", "fallback", "in4 paired planes", "in4 window moved left",
+                    "in4 idle waves", "fallback idle waves", "16 x 32 eight waves",
+                    "even K"}, seen
+
+
 def test_small_maps_take_small_tiles_and_many_waves():
     """7x7 outputs with 512 channels and filters: without dividing the
     channel sum among workgroups, filling the chip takes small tiles (at most

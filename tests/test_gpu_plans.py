@@ -10,6 +10,7 @@ import torch
 import paper_2212_00404_amd as dc
 from dconv_workloads import random_arrays
 from gpu_util import assert_exact, oracle_multi, oracle_single
+from private_layers import PRIVATE_LAYERS
 
 pytestmark = pytest.mark.gpu
 
@@ -26,6 +27,23 @@ def test_every_candidate_plan_is_exact(layer):
     It, Ft = torch.from_numpy(I).cuda(), torch.from_numpy(F).cuda()
     cands = dc.plan_multi_candidates(C, M, Wx, Wy, K)
     assert len(cands) >= 2
+    outs = [dc.multi(It, Ft, plan=p) for p in cands]
+    torch.cuda.synchronize()
+    for p, o in zip(cands, outs):
+        assert_exact(o.cpu().numpy(), O64, "%r plan %r" % (layer, p))
+
+
+@pytest.mark.parametrize("layer", PRIVATE_LAYERS, ids=[str(l) for l in PRIVATE_LAYERS])
+def test_private_stage_copy_forms_are_exact(layer):
+    """Every plan of the private-stage shapes (every wave covering the whole
+    tile) on layers that reach each of their copy forms."""
+    C, M, Wx, Wy, K = layer
+    I, F = random_arrays(C, M, Wx, Wy, K, seed=sum(layer) * 17 + 3, variant="int")
+    O64, _ = oracle_multi(I, F)
+    It, Ft = torch.from_numpy(I).cuda(), torch.from_numpy(F).cuda()
+    cands = [p for p in dc.plan_multi_candidates(C, M, Wx, Wy, K, "mfma")
+             if p["block"] // 64 == p["waves_c"]]
+    assert cands
     outs = [dc.multi(It, Ft, plan=p) for p in cands]
     torch.cuda.synchronize()
     for p, o in zip(cands, outs):
