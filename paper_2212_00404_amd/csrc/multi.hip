@@ -132,7 +132,7 @@ Candidate valu_candidate(int i) {
 // factor for several accumulator tiles per wave fitted to 1 and was
 // dropped); the MFMA terms are empirical weights, not instruction
 // latencies.
-double estimate(const Candidate &cd, bool mfma, int C, int M, int Wx, int K, int num_cu,
+double estimate(const Candidate &cd, bool mfma, int C, int M, int Wx, int Wy, int K, int num_cu,
                 const TileChoice &t, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
   const int64_t mtiles = (M + cd.MT - 1) / cd.MT;
@@ -152,7 +152,7 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int Wx, int K, int
   const bool priv = mfma && private_stages(cd);
   const int ics = priv ? mfma_ics(K, cd.PT, cd.mf) : 0;
   const int ih = t.tpy + K - 1, iwp = (t.tpx + K - 1 + 3) & ~3;
-  const bool in4 = priv && ics != 32 && Wx >= iwp && ih * iwp <= ics;
+  const bool in4 = priv && Wx >= iwp && ih * iwp <= ics && (int64_t)Wx * Wy < (1 << 24);
   const double kCopyBytesPerClock = in4 ? 12.1 : priv ? 12.8 : 11.7;
   const double kStageOverhead = mfma ? (in4 ? 294.0 : priv ? 410.0 : 652.0) : 300.0;
   const double kLatency = mfma ? 11.0 : 2000.0;
@@ -214,7 +214,7 @@ void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu
       lds_bytes = 4 * (stage > cd.red_floats ? stage : cd.red_floats);
     }
     if (lds_bytes > kMaxLds) continue;
-    const double tm = estimate(cd, mfma, C, M, Wx, K, num_cu, t, lds_bytes);
+    const double tm = estimate(cd, mfma, C, M, Wx, Wy, K, num_cu, t, lds_bytes);
     MultiPlan p{};
     p.variant = mfma ? DCONV_VARIANT_MFMA : DCONV_VARIANT_VALU;
     p.kernel = i;
