@@ -20,9 +20,13 @@ constexpr int kGenericKernel = 99;
 struct TileChoice { int tpy, tpx, tiles_x, tiles_y; int64_t lanes; };
 
 // Rectangular output tiles of at most `cap` pixels; pick the shape that
-// wastes the fewest pixel lanes over the whole map (ties: wider tiles, for
-// coalesced rows).
-TileChoice choose_tile(int Hout, int Wout, int cap) {
+// wastes the fewest pixel lanes over the whole map.  Ties go first (K > 1)
+// to a tile whose input row, padded to whole float4s, still fits in the
+// map width (the condition for 16-byte input copies), then to the wider
+// tile, for coalesced rows.
+TileChoice choose_tile(int Hout, int Wout, int cap, int K) {
+  const int Wx = Wout + K - 1;
+  const auto row_fits = [&](int tpx) { return K > 1 && ((tpx + K - 1 + 3) & ~3) <= Wx; };
   TileChoice best{1, 1, Wout, Hout, INT64_MAX};
   for (int tpx = 1; tpx <= cap && tpx <= Wout; ++tpx) {
     int tpy = cap / tpx;
@@ -31,7 +35,9 @@ TileChoice choose_tile(int Hout, int Wout, int cap) {
     const int tx = (Wout + tpx - 1) / tpx;
     const int ty = (Hout + tpy - 1) / tpy;
     const int64_t lanes = (int64_t)tx * ty * cap;
-    if (lanes < best.lanes || (lanes == best.lanes && tpx > best.tpx))
+    const bool fits = row_fits(tpx), bfits = row_fits(best.tpx);
+    if (lanes < best.lanes ||
+        (lanes == best.lanes && (fits > bfits || (fits == bfits && tpx > best.tpx))))
       best = TileChoice{tpy, tpx, tx, ty, lanes};
   }
   return best;
@@ -206,7 +212,7 @@ void enumerate_family(int C, int M, int Wx, int Wy, int K, bool mfma, int num_cu
          (int64_t)cd.MT * C * K * K >= (int64_t(1) << 30) ||
          (int64_t)(cd.CC / cd.WC) * Wx * Wy >= (int64_t(1) << 30)))
       continue;
-    const TileChoice t = choose_tile(Hout, Wout, cd.PT);
+    const TileChoice t = choose_tile(Hout, Wout, cd.PT, K);
     const int IH = t.tpy + K - 1, IW = t.tpx + K - 1;
     int64_t lds_bytes = cd.lds_fixed;
     if (!mfma) {
