@@ -132,12 +132,12 @@ Candidate valu_candidate(int i) {
 // have their own stage cost and copy rate.  The constants were fitted to
 // exhaustive timings of every matrix-core candidate plan of 21 benchmark
 // layers and 48 seeded random layers on an MI355X, the six bench-step
-// layers weighted five times (the fitted model picks the fastest plan on
-// five of those six, 1.14x on the sixth, 2.2% above the fastest on average
-// over all 69, 20% at worst; 2.6% and 17% on 24 other random layers; a
-// factor for several accumulator tiles per wave fitted to 1 and was
-// dropped); the MFMA terms are empirical weights, not instruction
-// latencies.
+// layers weighted five times (a factor for several accumulator tiles per
+// wave fitted to 1 and was dropped).  With the tile rule of choose_tile the
+// model picks the fastest plan on all six bench-step layers, is 1.7% above
+// the fastest on average over all 69 (30% at worst, a 1x1 layer) and 2.4%
+// on 24 other random layers (13% at worst).  The MFMA terms are empirical
+// weights, not instruction latencies.
 double estimate(const Candidate &cd, bool mfma, int C, int M, int Wx, int Wy, int K, int num_cu,
                 const TileChoice &t, int64_t lds_bytes) {
   const int64_t ntiles = (int64_t)t.tiles_x * t.tiles_y;
