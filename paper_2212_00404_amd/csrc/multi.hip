@@ -1,5 +1,6 @@
 // Multi-channel direct convolution: the planner (workgroup shape, output
 // tile, channels per stage, time model) and launch_multi (paper, Section 3.2).
+#include <algorithm>
 #include <cmath>
 #include <vector>
 
@@ -134,9 +135,9 @@ Candidate valu_candidate(int i) {
 // layers and 48 seeded random layers on an MI355X, the six bench-step
 // layers weighted five times (a factor for several accumulator tiles per
 // wave fitted to 1 and was dropped).  With the tile rule of choose_tile the
-// model picks the fastest plan on all six bench-step layers, is 1.7% above
-// the fastest on average over all 69 (30% at worst, a 1x1 layer) and 2.4%
-// on 24 other random layers (13% at worst).  The MFMA terms are empirical
+// model picks the fastest plan on all six bench-step layers, is 1.4% above
+// the fastest on average over all 69 (23% at worst) and 2.4% on 24 other
+// random layers (13% at worst).  The MFMA terms are empirical
 // weights, not instruction latencies.
 double estimate(const Candidate &cd, bool mfma, int C, int M, int Wx, int Wy, int K, int num_cu,
                 const TileChoice &t, int64_t lds_bytes) {
@@ -189,7 +190,19 @@ double estimate(const Candidate &cd, bool mfma, int C, int M, int Wx, int Wy, in
       mfma ? (double)per_cu * staged / (kCopyBytesPerClock * std::pow(wpc / 8.0, 0.05)) : 0.0;
   double tm = work > chain ? work : chain;
   if (copy > tm) tm = copy;
-  return tm + (cd.WC - 1) * kWcReduction + kLatency + kLaunch;
+  tm += (cd.WC - 1) * kWcReduction + kLatency + kLaunch;
+  // Private stages: in a last stage of fewer than CC channels the waves past
+  // them get none; the time grows by kIdleWaves times the share of wave
+  // stages left idle (fitted afterwards; it changes the plan of one
+  // benchmark layer of the 93 timed, a 1x1 layer with 64 channels).
+  if (priv) {
+    constexpr double kIdleWaves = 0.5;
+    const int rem = C % cd.CC ? C % cd.CC : cd.CC;
+    const int ccw = cd.CC / cd.WC;
+    const int active = std::min(cd.WC, (rem + ccw - 1) / ccw);
+    tm *= 1.0 + kIdleWaves * (double)(cd.WC - active) / cd.WC / stages;
+  }
+  return tm;
 }
 
 // Every workgroup shape of one family whose LDS footprint fits, with the
