@@ -161,6 +161,53 @@ def test_candidates_cover_the_planner_and_fit(layer):
         assert p["grid_x"] == tiles * -(-M // p["tile_m"])
 
 
+# Pixel lanes per workgroup tile of each matrix-core shape (MF x NB x WN).
+MFMA_TILE_PIXELS = [32, 128, 64, 128, 128, 64, 64, 128, 32, 32, 16, 16, 16, 16, 32, 32]
+
+
+@pytest.mark.parametrize("layer", MULTI_LAYERS + [(512, 512, 16, 16, 3), (512, 512, 7, 7, 3),
+                                                  (512, 512, 14, 14, 1), (37, 40, 33, 20, 3)])
+def test_tile_choice(layer):
+    """Each matrix-core candidate's output tile wastes the fewest pixel lanes
+    over the map; among such tiles it takes (K > 1) one whose input row,
+    padded to whole float4s, fits in the map width, then the widest."""
+    C, M, Wx, Wy, K = layer
+    if K > 11:
+        return
+    Hout, Wout = Wy - K + 1, Wx - K + 1
+    for p in dc.plan_multi_candidates(C, M, Wx, Wy, K, "mfma"):
+        cap = MFMA_TILE_PIXELS[p["kernel"]]
+        tiles = []
+        for tpx in range(1, min(cap, Wout) + 1):
+            tpy = min(cap // tpx, Hout)
+            lanes = -(-Wout // tpx) * -(-Hout // tpy) * cap
+            fits = K > 1 and (tpx + K - 1 + 3) // 4 * 4 <= Wx
+            tiles.append((lanes, not fits, -tpx, tpy, tpx))
+        best = min(tiles)
+        assert (p["tile_h"], p["tile_w"]) == (best[3], best[4]), (p, best)
+
+
+def test_tile_choice_examples():
+    """A 7x7 output of a 9x9 map takes 4x4 tiles of 16 pixels (rows of 6
+    floats, padded to 8, fit the map's 9; the equally wasteful 2x7 tile's 9,
+    padded to 12, do not); a 28x28 output, 2x16 tiles of 32 pixels rather
+    than 1x28; K = 1 keeps the widest tile."""
+    plans = {p["kernel"]: p for p in dc.plan_multi_candidates(512, 512, 9, 9, 3, "mfma")}
+    assert (plans[10]["tile_h"], plans[10]["tile_w"]) == (4, 4)
+    plans = {p["kernel"]: p for p in dc.plan_multi_candidates(256, 256, 30, 30, 3, "mfma")}
+    assert (plans[9]["tile_h"], plans[9]["tile_w"]) == (2, 16)
+    plans = {p["kernel"]: p for p in dc.plan_multi_candidates(256, 256, 28, 28, 1, "mfma")}
+    assert (plans[8]["tile_h"], plans[8]["tile_w"]) == (1, 28)
+
+
+def test_planner_avoids_idle_waves():
+    """With 64 channels, the deep 128-channel private shapes leave half their
+    waves without channels; the planner prices that and takes another
+    shape on the 56x56 1x1 layer."""
+    p = dc.plan_multi(64, 64, 56, 56, 1)
+    assert p["kernel"] not in (8, 9), p
+
+
 @pytest.mark.parametrize("layer", MULTI_LAYERS)
 def test_paper_rule_plan(layer):
     C, M, Wx, Wy, K = layer
