@@ -79,7 +79,11 @@ constexpr int kBlock = 256;
 // 24-bit multiply (a 32-bit one issues at a quarter of the rate).
 __device__ __forceinline__ int mul24(int a, int b) { return (int)__umul24(a, b); }
 
-// n / d for 0 <= n < 2^22 and 1 <= d < 2^11 using a float reciprocal.
+// n / d for 0 <= n < 2^16 and 1 <= d < 2^16 using a float reciprocal inv
+// within one ulp of 1/d (the hardware's approximate reciprocal, rcp(d)):
+// the truncated product is then off by at most one, which the remainder
+// test corrects.
+__device__ __forceinline__ float rcp(int d) { return __builtin_amdgcn_rcpf((float)d); }
 __device__ __forceinline__ int fdiv(int n, int d, float inv) {
   int q = __float2int_rz((float)n * inv);
   int r = n - q * d;
@@ -99,8 +103,8 @@ __device__ __forceinline__ void stage_input(float *__restrict__ Is, const float 
   constexpr int kBatch = 8;
   const int per_c = IH * IW;
   const int total = CC * per_c;
-  const float inv_pc = 1.0f / (float)per_c;
-  const float inv_iw = 1.0f / (float)IW;
+  const float inv_pc = rcp(per_c);
+  const float inv_iw = rcp(IW);
   for (int base = threadIdx.x; base < total; base += kBlock * kBatch) {
     float v[kBatch];
     int dst[kBatch];
@@ -447,7 +451,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   const int sx = in4 ? min(px0, a.Wx - IWP) : px0;
   // Divisions by run-time tile sizes through a float reciprocal (fdiv): the
   // integer division sequence costs tens of instructions per lane.
-  const float inv_tpx = 1.0f / (float)a.tpx;
+  const float inv_tpx = rcp(a.tpx);
   int b_base[NB];
   const int npix = a.tpy * a.tpx;
 #pragma unroll
@@ -480,7 +484,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   const int nci = PAIR ? 1 : (plane + 63) >> 6;
   // (Not used by the 16-byte input copies of private stages.)
   int ioff[NCI];
-  const float inv_iw = 1.0f / (float)a.IW;
+  const float inv_iw = rcp(a.IW);
   if (!in4) {
 #pragma unroll
     for (int j = 0; j < NCI; ++j) {
@@ -682,7 +686,7 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   uint32_t vin4[NC4 > 0 ? NC4 : 1], vint[NT4 > 0 ? NT4 : 1];
   int vpl4[NC4 > 0 ? NC4 : 1], vplt[NT4 > 0 ? NT4 : 1];
   bool it_ok[NT4 > 0 ? NT4 : 1];
-  const float inv_iwp = 1.0f / (float)IWP;
+  const float inv_iwp = rcp(IWP);
   const int plane_i = a.Wx * a.Wy;   // below 2^24 where IN4 holds
   auto in_src = [&](int e, uint32_t &vo, int &pl) __attribute__((always_inline)) {
     int i = e / ICS;
