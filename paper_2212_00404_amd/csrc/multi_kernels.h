@@ -822,7 +822,9 @@ __global__ __launch_bounds__(64 * WM * WN * WC) void multi_mfma(const float *__r
   // `mid` runs halfway through the chunks (the private stages' copies).
   auto compute = [&](const float *buf, auto &&mid) __attribute__((always_inline)) {
     constexpr int NQ = (CCW / KG) * KK;
-    constexpr int L = 4;
+    // chunks of 3 where they divide the k-steps and 4 do not (K = 3): 0.5%
+    // faster on average over the K = 3 plans
+    constexpr int L = (NQ % 4 != 0 && NQ % 3 == 0) ? 3 : 4;
     constexpr int NCH = (NQ + L - 1) / L;
     float ca[L][MB], cb[L][NB], na[L][MB], nbv[L][NB];
     auto load_chunk = [&](int ch, float (&av)[L][MB], float (&bv)[L][NB]) {
